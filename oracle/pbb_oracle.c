@@ -1,0 +1,243 @@
+/*
+ * Plain fp64 CPU oracle for Post-Boundary Bridge (PBB) decode attention.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing on the product path may link, load or call this
+ * file: only the test suite, the smoke check and the benchmark's CPU-baseline leg use it.
+ * It shares no code, header or constant with the HIP library.
+ *
+ * What it computes (paper: "Post-Boundary Bridge: Must Local Attention Go Global
+ * Between Global Layers?"):
+ *   - block geometry p(t) = b*floor(t/b), r(t) = t - p(t)                 Sec. 2.2, Eq.(1)
+ *   - the PBB support in its two-case form:                               Sec. 3, Eq.(pbb)
+ *       A(t) = {p..t}  union  {p-h..p-1} if p > 0 and 0 <= r < h, else nothing
+ *   - the sliding-window support {max(0,t-w+1)..t}                         Prop. 2 (Sec. 2.2)
+ *   - single-softmax attention over a support, scores q.k/sqrt(d)          Sec. 3, Eq.(attention)
+ * Keys and values are read from HISTORY arrays indexed by absolute position, never from
+ * a ring, and every sum is taken in fp64 in plain position order.
+ */
+#include <math.h>
+#include <pthread.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#include <unistd.h>
+
+/* Membership of source s in the PBB support of target t (Eq.(pbb), two-case form). */
+int oracle_pbb_member(int64_t t, int64_t s, int64_t block, int64_t bridge) {
+    if (s < 0 || s > t) return 0;
+    int64_t p = block * (t / block); /* block start, Eq.(1) */
+    int64_t r = t - p;               /* target phase, Eq.(1) */
+    if (s >= p) return 1;            /* causal block prefix {p..t} */
+    if (p > 0 && r < bridge && s >= p - bridge && s <= p - 1) return 1; /* bridge */
+    return 0;
+}
+
+/* Membership of source s in the sliding-window support of t (window includes t). */
+int oracle_swa_member(int64_t t, int64_t s, int64_t window) {
+    int64_t lo = t - window + 1;
+    if (lo < 0) lo = 0;
+    return s >= lo && s <= t;
+}
+
+/*
+ * Unique-score counts over a length-n sequence (Appendix A.5, "Exact arithmetic matching"):
+ * total = sum_t |A(t)|; cross = number of (t,s) pairs with s < p(t), i.e. sources in an
+ * earlier block (block size `block` defines p).  Brute force over every (t, s) pair in a
+ * window wide enough to hold the support; each membership is the definition above.
+ */
+void oracle_pbb_counts(int64_t n, int64_t block, int64_t bridge, int64_t *total, int64_t *cross) {
+    int64_t tot = 0, cr = 0;
+    for (int64_t t = 0; t < n; ++t) {
+        int64_t p = block * (t / block);
+        int64_t lo = p - bridge;
+        if (lo < 0) lo = 0;
+        for (int64_t s = lo; s <= t; ++s) {
+            if (oracle_pbb_member(t, s, block, bridge)) {
+                ++tot;
+                if (s < p) ++cr;
+            }
+        }
+    }
+    *total = tot;
+    *cross = cr;
+}
+
+void oracle_swa_counts(int64_t n, int64_t window, int64_t block, int64_t *total, int64_t *cross) {
+    int64_t tot = 0, cr = 0;
+    for (int64_t t = 0; t < n; ++t) {
+        int64_t p = block * (t / block);
+        int64_t lo = t - window;
+        if (lo < 0) lo = 0;
+        for (int64_t s = lo; s <= t; ++s) {
+            if (oracle_swa_member(t, s, window)) {
+                ++tot;
+                if (s < p) ++cr;
+            }
+        }
+    }
+    *total = tot;
+    *cross = cr;
+}
+
+/*
+ * Single-softmax attention of one query over an explicit list of n keys (Eq.(attention)):
+ *   z_s = scale * sum_c q[c] k[s][c];  o = sum_s e^{z_s} v_s / sum_s e^{z_s}.
+ * The maximum score is subtracted before exponentiation (this changes no result).
+ * Writes o[d] and, if lse != NULL, the log-partition log(sum_s e^{z_s}).
+ * n == 0 writes zeros and lse = -inf (an empty support has Z = 0, Appendix A.4, Eq.(lse)).
+ */
+void oracle_attend(int64_t n, int64_t d, const double *q, const double *k, const double *v,
+                   double scale, double *o, double *lse) {
+    for (int64_t c = 0; c < d; ++c) o[c] = 0.0;
+    if (n <= 0) {
+        if (lse) *lse = -INFINITY;
+        return;
+    }
+    double *z = (double *)malloc(sizeof(double) * (size_t)n);
+    double m = -INFINITY;
+    for (int64_t s = 0; s < n; ++s) {
+        double acc = 0.0;
+        for (int64_t c = 0; c < d; ++c) acc += q[c] * k[s * d + c];
+        z[s] = acc * scale;
+        if (z[s] > m) m = z[s];
+    }
+    double den = 0.0;
+    for (int64_t s = 0; s < n; ++s) {
+        double w = exp(z[s] - m);
+        den += w;
+        for (int64_t c = 0; c < d; ++c) o[c] += w * v[s * d + c];
+    }
+    for (int64_t c = 0; c < d; ++c) o[c] /= den;
+    if (lse) *lse = m + log(den);
+    free(z);
+}
+
+/* ------------------------------------------------------------------------------------ */
+/* Batched decode over absolute-position history.                                        */
+
+typedef struct {
+    int mode; /* 0 = PBB, 1 = SWA */
+    int64_t batch, n_q_heads, n_kv_heads, head_dim, block, window;
+    const int64_t *pos;
+    const float *q;      /* [batch][Hq][d] */
+    const float *k_hist; /* [batch][Hkv][hist_len][d], position s at row s - hist_lo[b] */
+    const float *v_hist;
+    const int64_t *hist_lo;
+    int64_t hist_len;
+    double scale;
+    double *out; /* [batch][Hq][d] */
+    int64_t next;       /* next (b, head) work item */
+    int error;
+    pthread_mutex_t lock;
+} decode_job;
+
+static int member(const decode_job *j, int64_t t, int64_t s) {
+    if (j->mode == 0) return oracle_pbb_member(t, s, j->block, j->block / 2);
+    return oracle_swa_member(t, s, j->window);
+}
+
+static void decode_one(decode_job *j, int64_t item, double *z, double *qd) {
+    const int64_t d = j->head_dim;
+    const int64_t G = j->n_q_heads / j->n_kv_heads;
+    const int64_t b = item / j->n_q_heads, i = item % j->n_q_heads;
+    const int64_t g = i / G; /* query head i reads KV head floor(i/G) */
+    const int64_t t = j->pos[b];
+    double *o = j->out + (b * j->n_q_heads + i) * d;
+    for (int64_t c = 0; c < d; ++c) o[c] = 0.0;
+    if (t < 0) return;
+    for (int64_t c = 0; c < d; ++c) qd[c] = (double)j->q[(b * j->n_q_heads + i) * d + c];
+    /* Candidate window: wide enough to contain every source either definition admits. */
+    int64_t span = (j->mode == 0) ? (j->block + j->block / 2) : j->window;
+    int64_t lo = t - span;
+    if (lo < 0) lo = 0;
+    const float *kh = j->k_hist + (b * j->n_kv_heads + g) * j->hist_len * d;
+    const float *vh = j->v_hist + (b * j->n_kv_heads + g) * j->hist_len * d;
+    double m = -INFINITY;
+    int64_t cnt = 0;
+    for (int64_t s = lo; s <= t; ++s) {
+        if (!member(j, t, s)) continue;
+        int64_t row = s - j->hist_lo[b];
+        if (row < 0 || row >= j->hist_len) {
+            j->error = 1; /* the caller did not supply this history position */
+            return;
+        }
+        double acc = 0.0;
+        for (int64_t c = 0; c < d; ++c) acc += qd[c] * (double)kh[row * d + c];
+        z[s - lo] = acc * j->scale;
+        if (z[s - lo] > m) m = z[s - lo];
+        ++cnt;
+    }
+    double den = 0.0;
+    for (int64_t s = lo; s <= t; ++s) {
+        if (!member(j, t, s)) continue;
+        int64_t row = s - j->hist_lo[b];
+        double w = exp(z[s - lo] - m);
+        den += w;
+        for (int64_t c = 0; c < d; ++c) o[c] += w * (double)vh[row * d + c];
+    }
+    (void)cnt;
+    for (int64_t c = 0; c < d; ++c) o[c] /= den;
+}
+
+static void *decode_worker(void *arg) {
+    decode_job *j = (decode_job *)arg;
+    int64_t span = (j->mode == 0) ? (j->block + j->block / 2) : j->window;
+    double *z = (double *)malloc(sizeof(double) * (size_t)(span + 1));
+    double *qd = (double *)malloc(sizeof(double) * (size_t)j->head_dim);
+    const int64_t total = j->batch * j->n_q_heads;
+    for (;;) {
+        pthread_mutex_lock(&j->lock);
+        int64_t item = j->next;
+        j->next += 1;
+        pthread_mutex_unlock(&j->lock);
+        if (item >= total) break;
+        decode_one(j, item, z, qd);
+    }
+    free(z);
+    free(qd);
+    return NULL;
+}
+
+/*
+ * One decode step for a batch: for every sequence b and query head i, attention of
+ * q[b][i] over the support of t = pos[b] (PBB with h = block/2 when mode == 0, SWA with
+ * the given window when mode == 1).  Returns 0 on success, 1 if some needed history
+ * position lies outside [hist_lo[b], hist_lo[b] + hist_len), 2 on bad arguments.
+ * n_threads <= 0 uses every online core.
+ */
+int oracle_decode(int mode, int64_t batch, int64_t n_q_heads, int64_t n_kv_heads,
+                  int64_t head_dim, int64_t block, int64_t window, const int64_t *pos,
+                  const float *q, const float *k_hist, const float *v_hist,
+                  const int64_t *hist_lo, int64_t hist_len, double scale, double *out,
+                  int n_threads) {
+    if (batch < 0 || n_q_heads <= 0 || n_kv_heads <= 0 || head_dim <= 0) return 2;
+    if (n_q_heads % n_kv_heads != 0) return 2;
+    if (mode == 0 && (block < 2 || block % 2 != 0)) return 2;
+    if (mode == 1 && window < 1) return 2;
+    decode_job j;
+    memset(&j, 0, sizeof(j));
+    j.mode = mode;
+    j.batch = batch;
+    j.n_q_heads = n_q_heads;
+    j.n_kv_heads = n_kv_heads;
+    j.head_dim = head_dim;
+    j.block = block;
+    j.window = window;
+    j.pos = pos;
+    j.q = q;
+    j.k_hist = k_hist;
+    j.v_hist = v_hist;
+    j.hist_lo = hist_lo;
+    j.hist_len = hist_len;
+    j.scale = scale;
+    j.out = out;
+    pthread_mutex_init(&j.lock, NULL);
+    if (n_threads <= 0) n_threads = (int)sysconf(_SC_NPROCESSORS_ONLN);
+    if (n_threads < 1) n_threads = 1;
+    if (n_threads > 256) n_threads = 256;
+    pthread_t th[256];
+    for (int i = 0; i < n_threads; ++i) pthread_create(&th[i], NULL, decode_worker, &j);
+    for (int i = 0; i < n_threads; ++i) pthread_join(th[i], NULL);
+    pthread_mutex_destroy(&j.lock);
+    return j.error ? 1 : 0;
+}
