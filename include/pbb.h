@@ -1,0 +1,148 @@
+/*
+ * pbb.h -- C ABI of libpbb: Post-Boundary Bridge (PBB) decode attention on AMD Instinct
+ * MI355X (gfx950), with a sliding-window (SWA) ring baseline built on the same kernels.
+ *
+ * Method (paper: "Post-Boundary Bridge: Must Local Attention Go Global Between Global
+ * Layers?"):
+ *   - A target at absolute position t sits in block p = B*floor(t/B) at phase r = t - p
+ *     (Sec. 2.2, Eq.(1)).  Its PBB support is the causal block prefix {p..t}, plus the
+ *     preceding half-block {p-h..p-1} when p > 0 and r < h, with h = B/2 (Sec. 3, Eq.(pbb)).
+ *   - The output is one softmax over that support with scores q.k * scale, scale = 1/sqrt(d)
+ *     by default (Sec. 3, Eq.(attention)); query head i reads KV head floor(i/G), G = Hq/Hkv
+ *     (native grouped-query attention, Sec. 3 and Appendix F.1).
+ *   - Keys and values live in a ring of B slots per (sequence, KV head): position s is stored
+ *     at slot s mod B, so an append overwrites only a position that no current or future
+ *     support needs and retained entries never move (Sec. 3 "Flash-PBB"; Appendix F.1,
+ *     Proposition "Relocation-free PBB cache").
+ *   - The SWA baseline attends over {max(0, t-W+1) .. t} (Prop. 2, Sec. 2.2) stored in a
+ *     ring of S >= W slots (Appendix F.1: a sliding window also admits a ring).
+ *
+ * Layouts (row-major, contiguous, element type given by pbb_desc_t.dtype):
+ *   q, out          [batch][n_q_heads][head_dim]
+ *   k_new, v_new    [batch][n_kv_heads][head_dim]       key/value of the token at pos[b]
+ *   k_ring, v_ring  [batch][n_kv_heads][slots][head_dim]
+ *   pos             int32 [batch], 0 <= pos[b] < 2^31 - 1 (device memory)
+ * Every pointer is DEVICE memory of the current HIP device and must be 16-byte aligned
+ * (pos: 4-byte aligned).  A negative pos[b] makes that sequence's output zero and skips its
+ * append.  Aliasing between any two buffers is undefined.
+ *
+ * Ownership: the caller allocates and frees every buffer, including the workspace.  The
+ * library allocates nothing, keeps no pointer after a call returns, holds no global state
+ * and is re-entrant.  Calls that take a stream only enqueue work on it (asynchronous); the
+ * stream argument is a hipStream_t (NULL = the null stream).
+ *
+ * Errors: every entry point returns a pbb_status_t.  Arguments are checked on the host
+ * before anything is enqueued; on any error nothing is launched and nothing is written.
+ * No entry point aborts, prints, or lets a C++ exception escape.  PBB_ERR_LAUNCH reports a
+ * failure returned by the HIP runtime when enqueueing.
+ */
+#ifndef PBB_H_
+#define PBB_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  PBB_OK = 0,
+  PBB_ERR_NULL = 1,      /* a required pointer is NULL */
+  PBB_ERR_SHAPE = 2,     /* inconsistent or unsupported sizes (see pbb_desc_t) */
+  PBB_ERR_DTYPE = 3,     /* unsupported element type */
+  PBB_ERR_ALIGN = 4,     /* a pointer is not 16-byte aligned (pos: 4-byte) */
+  PBB_ERR_WORKSPACE = 5, /* workspace smaller than the size query returns */
+  PBB_ERR_LAUNCH = 6     /* the HIP runtime refused the launch */
+} pbb_status_t;
+
+typedef enum {
+  PBB_DTYPE_F32 = 0,  /* float32 inputs and outputs, float32 arithmetic throughout */
+  PBB_DTYPE_BF16 = 1  /* bfloat16 inputs and outputs; fp32 accumulation; RNE on store */
+} pbb_dtype_t;
+
+/*
+ * Problem description.  Constraints (PBB_ERR_SHAPE otherwise):
+ *   batch >= 1; n_kv_heads >= 1; n_q_heads a multiple of n_kv_heads with
+ *   G = n_q_heads / n_kv_heads <= 16; head_dim in {64, 128};
+ *   PBB: block even, 2 <= block <= 65536, slots == block (the ring has exactly B slots);
+ *   SWA: 1 <= window <= slots <= 65536 (block is ignored).
+ * scale <= 0 selects 1/sqrt(head_dim) (Sec. 3, Eq.(attention)).
+ */
+typedef struct {
+  int32_t batch;
+  int32_t n_q_heads;
+  int32_t n_kv_heads;
+  int32_t head_dim;
+  int32_t block;   /* PBB block size B; bridge width h = B/2 */
+  int32_t window;  /* SWA window W (includes the current token); 0 for PBB */
+  int32_t slots;   /* ring slots per (sequence, KV head) */
+  int32_t dtype;   /* a pbb_dtype_t */
+  float scale;
+} pbb_desc_t;
+
+/* Human-readable name of a status code (static storage; never NULL). */
+const char *pbb_status_string(pbb_status_t status);
+
+/*
+ * Bytes of ONE ring tensor (K or V): batch * n_kv_heads * slots * head_dim * element size.
+ * The paper's local KV storage, 2 * batch * B * H_KV * d_h * u, is twice this for the PBB
+ * ring (Appendix F.1).  Validates desc as pbb_decode_step would (SWA rules when window > 0).
+ */
+pbb_status_t pbb_ring_bytes(const pbb_desc_t *desc, size_t *bytes_per_tensor);
+
+/*
+ * Enqueue zero-filling of both rings on `stream`.  A zeroed ring is the state before the
+ * first decode step at position 0: for t < slots the support only covers positions that
+ * have been appended, so the zeros are never read (Appendix F.1, proof of the proposition).
+ */
+pbb_status_t pbb_ring_init(const pbb_desc_t *desc, void *k_ring, void *v_ring, void *stream);
+
+/*
+ * Enqueue a bulk load of history into the rings (the state a prefill leaves behind).
+ * k_src, v_src: [batch][n_kv_heads][src_len][head_dim], row i holding absolute position
+ * pos[b] - src_len + i of sequence b.  Each row with a non-negative position s is copied bit
+ * for bit to slot s mod slots (Appendix F.1); rows with negative positions are skipped, as
+ * are sequences with pos[b] < 0.  Requires 0 <= src_len <= slots.  pos is not modified: after
+ * the call the rings hold exactly what sequential appends of those positions would leave.
+ */
+pbb_status_t pbb_ring_fill(const pbb_desc_t *desc, const int32_t *pos, const void *k_src,
+                           const void *v_src, int32_t src_len, void *k_ring, void *v_ring,
+                           void *stream);
+
+/* Workspace bytes pbb_decode_step needs (0 when the selected kernel needs none). */
+pbb_status_t pbb_workspace_bytes(const pbb_desc_t *desc, size_t *bytes);
+
+/*
+ * One PBB decode step for every sequence, fused in a single kernel launch:
+ *   1. append: k_ring[b][g][t mod B] <- k_new[b][g], same for V, t = pos[b]
+ *      (Sec. 3 "Flash-PBB"; the overwritten position t - B is outside A(t), Appendix F.1);
+ *   2. attention: out[b][i] = softmax over s in A_PBB(t) of (q[b][i] . k_s * scale) applied
+ *      to v_s, for every query head i, with k_t, v_t taken from k_new, v_new
+ *      (Eq.(pbb) with h = B/2, Eq.(attention)).
+ * Requires slots == block and window ignored.  pos is read, never written: the caller
+ * advances it (for example pos += 1 on the same stream) before the next step.
+ * workspace may be NULL when pbb_workspace_bytes reports 0.
+ */
+pbb_status_t pbb_decode_step(const pbb_desc_t *desc, const int32_t *pos, const void *q,
+                             const void *k_new, const void *v_new, void *k_ring, void *v_ring,
+                             void *out, void *workspace, size_t workspace_bytes, void *stream);
+
+/* Workspace bytes swa_decode_step needs (0 when the selected kernel needs none). */
+pbb_status_t swa_workspace_bytes(const pbb_desc_t *desc, size_t *bytes);
+
+/*
+ * Sliding-window baseline with the same arguments: appends at slot t mod slots and attends
+ * over {max(0, t-W+1) .. t} (Prop. 2), W = desc->window, read from a ring of desc->slots >= W
+ * entries.  The overwritten position t - slots lies before the window, so no read races the
+ * append.
+ */
+pbb_status_t swa_decode_step(const pbb_desc_t *desc, const int32_t *pos, const void *q,
+                             const void *k_new, const void *v_new, void *k_ring, void *v_ring,
+                             void *out, void *workspace, size_t workspace_bytes, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PBB_H_ */

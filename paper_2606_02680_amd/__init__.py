@@ -1,0 +1,8 @@
+"""MI355X-native Post-Boundary Bridge (PBB) decode attention.
+
+The product is ``libpbb.so`` (C ABI in ``include/pbb.h``, HIP kernels for gfx950 in
+``csrc/``); :mod:`paper_2606_02680_amd.pbb` is its thin ctypes binding.
+"""
+from .pbb import (  # noqa: F401
+    PbbDesc, PbbError, alloc_rings, load_library, make_desc, pbb_decode_step, ring_bytes,
+    ring_fill, ring_init, swa_decode_step, swa_workspace_bytes, workspace_bytes)

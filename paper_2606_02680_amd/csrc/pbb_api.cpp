@@ -1,0 +1,171 @@
+// C ABI of libpbb (declared in include/pbb.h): argument validation, kernel selection and
+// launch.  Every check runs on the host before anything is enqueued, so a failing call
+// launches nothing and writes nothing.  No exception crosses the ABI.
+
+#include "pbb.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+
+#include "pbb_internal.h"
+
+namespace {
+
+constexpr int32_t kMaxGroup = 16;     // query heads per KV head held by one MFMA tile
+constexpr int32_t kMaxSlots = 65536;  // ring slots per (sequence, KV head)
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+size_t elem_bytes(int32_t dtype) { return dtype == PBB_DTYPE_F32 ? 4 : 2; }
+
+// Shape rules shared by every entry point; `swa` selects the sliding-window rules.
+pbb_status_t check_desc(const pbb_desc_t* d, bool swa) {
+  if (d == nullptr) return PBB_ERR_NULL;
+  if (d->dtype != PBB_DTYPE_F32 && d->dtype != PBB_DTYPE_BF16) return PBB_ERR_DTYPE;
+  if (d->batch < 1 || d->n_kv_heads < 1 || d->n_q_heads < 1) return PBB_ERR_SHAPE;
+  if (d->n_q_heads % d->n_kv_heads != 0) return PBB_ERR_SHAPE;
+  if (d->n_q_heads / d->n_kv_heads > kMaxGroup) return PBB_ERR_SHAPE;
+  if (d->head_dim != 64 && d->head_dim != 128) return PBB_ERR_SHAPE;
+  if (swa) {
+    if (d->window < 1 || d->slots < d->window || d->slots > kMaxSlots) return PBB_ERR_SHAPE;
+  } else {
+    if (d->block < 2 || (d->block % 2) != 0 || d->block > kMaxSlots) return PBB_ERR_SHAPE;
+    if (d->slots != d->block) return PBB_ERR_SHAPE;
+  }
+  // Ring element counts must fit comfortably in 64-bit offsets and the launch grid.
+  const uint64_t rows = (uint64_t)d->batch * (uint64_t)d->n_kv_heads;
+  if (rows > 0x7fffffffull) return PBB_ERR_SHAPE;
+  return PBB_OK;
+}
+
+bool is_swa(const pbb_desc_t* d) { return d != nullptr && d->window > 0; }
+
+size_t ring_tensor_bytes(const pbb_desc_t* d) {
+  return (size_t)d->batch * (size_t)d->n_kv_heads * (size_t)d->slots * (size_t)d->head_dim *
+         elem_bytes(d->dtype);
+}
+
+pbb_status_t decode_common(const pbb_desc_t* desc, bool swa, const int32_t* pos, const void* q,
+                           const void* k_new, const void* v_new, void* k_ring, void* v_ring,
+                           void* out, void* workspace, size_t workspace_bytes, void* stream) {
+  (void)workspace;
+  (void)workspace_bytes;  // the selected kernels need no workspace
+  const pbb_status_t st = check_desc(desc, swa);
+  if (st != PBB_OK) return st;
+  if (!pos || !q || !k_new || !v_new || !k_ring || !v_ring || !out) return PBB_ERR_NULL;
+  if (!aligned(pos, 4) || !aligned(q, 16) || !aligned(k_new, 16) || !aligned(v_new, 16) ||
+      !aligned(k_ring, 16) || !aligned(v_ring, 16) || !aligned(out, 16))
+    return PBB_ERR_ALIGN;
+
+  pbb::DecodeArgs a;
+  a.pos = pos;
+  a.q = q;
+  a.k_new = k_new;
+  a.v_new = v_new;
+  a.k_ring = k_ring;
+  a.v_ring = v_ring;
+  a.out = out;
+  a.batch = desc->batch;
+  a.hq = desc->n_q_heads;
+  a.hkv = desc->n_kv_heads;
+  a.group = desc->n_q_heads / desc->n_kv_heads;
+  a.slots = desc->slots;
+  a.block = desc->block;
+  a.window = desc->window;
+  a.mode = swa ? pbb::kSupportSWA : pbb::kSupportPBB;
+  const float scale = desc->scale > 0.0f ? desc->scale
+                                         : (float)(1.0 / std::sqrt((double)desc->head_dim));
+  a.scale_log2 = (float)((double)scale * 1.4426950408889634);  // log2(e)
+
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const hipError_t e = desc->dtype == PBB_DTYPE_BF16 ? pbb::launch_decode_bf16(a, desc->head_dim, s)
+                                                     : pbb::launch_decode_f32(a, desc->head_dim, s);
+  return e == hipSuccess ? PBB_OK : PBB_ERR_LAUNCH;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* pbb_status_string(pbb_status_t status) {
+  switch (status) {
+    case PBB_OK: return "PBB_OK";
+    case PBB_ERR_NULL: return "PBB_ERR_NULL: a required pointer is NULL";
+    case PBB_ERR_SHAPE: return "PBB_ERR_SHAPE: inconsistent or unsupported sizes";
+    case PBB_ERR_DTYPE: return "PBB_ERR_DTYPE: unsupported element type";
+    case PBB_ERR_ALIGN: return "PBB_ERR_ALIGN: pointer not 16-byte aligned (pos: 4-byte)";
+    case PBB_ERR_WORKSPACE: return "PBB_ERR_WORKSPACE: workspace too small";
+    case PBB_ERR_LAUNCH: return "PBB_ERR_LAUNCH: the HIP runtime refused the launch";
+  }
+  return "PBB_ERR_UNKNOWN";
+}
+
+pbb_status_t pbb_ring_bytes(const pbb_desc_t* desc, size_t* bytes_per_tensor) {
+  if (desc == nullptr || bytes_per_tensor == nullptr) return PBB_ERR_NULL;
+  const pbb_status_t st = check_desc(desc, is_swa(desc));
+  if (st != PBB_OK) return st;
+  *bytes_per_tensor = ring_tensor_bytes(desc);
+  return PBB_OK;
+}
+
+pbb_status_t pbb_ring_init(const pbb_desc_t* desc, void* k_ring, void* v_ring, void* stream) {
+  const pbb_status_t st = check_desc(desc, is_swa(desc));
+  if (st != PBB_OK) return st;
+  if (!k_ring || !v_ring) return PBB_ERR_NULL;
+  if (!aligned(k_ring, 16) || !aligned(v_ring, 16)) return PBB_ERR_ALIGN;
+  const hipError_t e = pbb::launch_ring_zero(k_ring, v_ring, ring_tensor_bytes(desc),
+                                             reinterpret_cast<hipStream_t>(stream));
+  return e == hipSuccess ? PBB_OK : PBB_ERR_LAUNCH;
+}
+
+pbb_status_t pbb_ring_fill(const pbb_desc_t* desc, const int32_t* pos, const void* k_src,
+                           const void* v_src, int32_t src_len, void* k_ring, void* v_ring,
+                           void* stream) {
+  const pbb_status_t st = check_desc(desc, is_swa(desc));
+  if (st != PBB_OK) return st;
+  if (src_len < 0 || src_len > desc->slots) return PBB_ERR_SHAPE;
+  if (!pos || !k_ring || !v_ring) return PBB_ERR_NULL;
+  if (src_len > 0 && (!k_src || !v_src)) return PBB_ERR_NULL;
+  if (!aligned(pos, 4) || !aligned(k_ring, 16) || !aligned(v_ring, 16) ||
+      (src_len > 0 && (!aligned(k_src, 16) || !aligned(v_src, 16))))
+    return PBB_ERR_ALIGN;
+  const int32_t row_bytes = desc->head_dim * (int32_t)elem_bytes(desc->dtype);
+  const hipError_t e = pbb::launch_ring_fill(pos, k_src, v_src, k_ring, v_ring, desc->batch,
+                                             desc->n_kv_heads, src_len, desc->slots, row_bytes,
+                                             reinterpret_cast<hipStream_t>(stream));
+  return e == hipSuccess ? PBB_OK : PBB_ERR_LAUNCH;
+}
+
+pbb_status_t pbb_workspace_bytes(const pbb_desc_t* desc, size_t* bytes) {
+  if (desc == nullptr || bytes == nullptr) return PBB_ERR_NULL;
+  const pbb_status_t st = check_desc(desc, false);
+  if (st != PBB_OK) return st;
+  *bytes = 0;
+  return PBB_OK;
+}
+
+pbb_status_t swa_workspace_bytes(const pbb_desc_t* desc, size_t* bytes) {
+  if (desc == nullptr || bytes == nullptr) return PBB_ERR_NULL;
+  const pbb_status_t st = check_desc(desc, true);
+  if (st != PBB_OK) return st;
+  *bytes = 0;
+  return PBB_OK;
+}
+
+pbb_status_t pbb_decode_step(const pbb_desc_t* desc, const int32_t* pos, const void* q,
+                             const void* k_new, const void* v_new, void* k_ring, void* v_ring,
+                             void* out, void* workspace, size_t workspace_bytes, void* stream) {
+  return decode_common(desc, false, pos, q, k_new, v_new, k_ring, v_ring, out, workspace,
+                       workspace_bytes, stream);
+}
+
+pbb_status_t swa_decode_step(const pbb_desc_t* desc, const int32_t* pos, const void* q,
+                             const void* k_new, const void* v_new, void* k_ring, void* v_ring,
+                             void* out, void* workspace, size_t workspace_bytes, void* stream) {
+  return decode_common(desc, true, pos, q, k_new, v_new, k_ring, v_ring, out, workspace,
+                       workspace_bytes, stream);
+}
+
+}  // extern "C"

@@ -1,0 +1,47 @@
+// Internal interface between the C-ABI layer (pbb_api.cpp) and the HIP kernels
+// (pbb_kernels.hip).  Not installed; not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace pbb {
+
+enum SupportMode : int32_t { kSupportPBB = 0, kSupportSWA = 1 };
+
+// Everything a decode kernel needs, validated on the host before launch.
+struct DecodeArgs {
+  const int32_t* pos;
+  const void* q;
+  const void* k_new;
+  const void* v_new;
+  void* k_ring;
+  void* v_ring;
+  void* out;
+  int32_t batch;
+  int32_t hq;
+  int32_t hkv;
+  int32_t group;       // query heads per KV head, 1..16
+  int32_t slots;       // ring slots per (sequence, KV head)
+  int32_t block;       // PBB block size B
+  int32_t window;      // SWA window W
+  int32_t mode;        // SupportMode
+  float scale_log2;    // softmax scale times log2(e)
+};
+
+hipError_t launch_ring_zero(void* k_ring, void* v_ring, size_t bytes_per_tensor,
+                            hipStream_t stream);
+
+hipError_t launch_ring_fill(const int32_t* pos, const void* k_src, const void* v_src,
+                            void* k_ring, void* v_ring, int32_t batch, int32_t hkv,
+                            int32_t src_len, int32_t slots, int32_t row_bytes,
+                            hipStream_t stream);
+
+// bf16 decode on matrix cores; head_dim 64 or 128.
+hipError_t launch_decode_bf16(const DecodeArgs& a, int32_t head_dim, hipStream_t stream);
+
+// fp32 decode on vector ALUs; head_dim 64 or 128.
+hipError_t launch_decode_f32(const DecodeArgs& a, int32_t head_dim, hipStream_t stream);
+
+}  // namespace pbb

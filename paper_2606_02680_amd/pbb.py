@@ -1,0 +1,207 @@
+"""ctypes binding of libpbb (``include/pbb.h``).
+
+Argument marshalling only: every function checks that the tensors match the descriptor
+(device, dtype, shape, contiguity), passes raw device pointers and the current HIP stream of
+PyTorch to the C entry point of the same name, and raises :class:`PbbError` on a non-OK
+status.  All computation happens in the library's HIP kernels; there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+
+import torch
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpbb.so")
+
+PBB_OK = 0
+STATUS_NAMES = {0: "PBB_OK", 1: "PBB_ERR_NULL", 2: "PBB_ERR_SHAPE", 3: "PBB_ERR_DTYPE",
+                4: "PBB_ERR_ALIGN", 5: "PBB_ERR_WORKSPACE", 6: "PBB_ERR_LAUNCH"}
+DTYPE_F32 = 0
+DTYPE_BF16 = 1
+_TORCH_DTYPE = {DTYPE_F32: torch.float32, DTYPE_BF16: torch.bfloat16}
+
+EXPORTS = ("pbb_status_string", "pbb_ring_bytes", "pbb_ring_init", "pbb_ring_fill",
+           "pbb_workspace_bytes", "pbb_decode_step", "swa_workspace_bytes", "swa_decode_step")
+
+
+class PbbError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        self.status = status
+        super().__init__(f"{fn}: {STATUS_NAMES.get(status, status)} ({lib_status_string(status)})")
+
+
+class PbbDesc(ctypes.Structure):
+    """Mirror of ``pbb_desc_t``."""
+    _fields_ = [("batch", ctypes.c_int32), ("n_q_heads", ctypes.c_int32),
+                ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("block", ctypes.c_int32), ("window", ctypes.c_int32),
+                ("slots", ctypes.c_int32), ("dtype", ctypes.c_int32), ("scale", ctypes.c_float)]
+
+    @property
+    def torch_dtype(self) -> torch.dtype:
+        return _TORCH_DTYPE[self.dtype]
+
+    @property
+    def group(self) -> int:
+        return self.n_q_heads // self.n_kv_heads
+
+
+_lib = None
+
+
+def load_library(path: str = _LIB_PATH):
+    """Load libpbb.so; raises if it has not been built (no silent fallback)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise ImportError(f"libpbb.so not found at {path}: build it with "
+                          "`python -m paper_2606_02680_amd.build`")
+    lib = ctypes.CDLL(path)
+    vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+    dp = ctypes.POINTER(PbbDesc)
+    lib.pbb_status_string.argtypes = [ctypes.c_int]
+    lib.pbb_status_string.restype = ctypes.c_char_p
+    lib.pbb_ring_bytes.argtypes = [dp, ctypes.POINTER(sz)]
+    lib.pbb_ring_init.argtypes = [dp, vp, vp, vp]
+    lib.pbb_ring_fill.argtypes = [dp, vp, vp, vp, i32, vp, vp, vp]
+    lib.pbb_workspace_bytes.argtypes = [dp, ctypes.POINTER(sz)]
+    lib.swa_workspace_bytes.argtypes = [dp, ctypes.POINTER(sz)]
+    for fn in ("pbb_decode_step", "swa_decode_step"):
+        getattr(lib, fn).argtypes = [dp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    for fn in EXPORTS[1:]:
+        getattr(lib, fn).restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def lib_status_string(status: int) -> str:
+    return load_library().pbb_status_string(int(status)).decode()
+
+
+def make_desc(batch: int, n_q_heads: int, n_kv_heads: int, head_dim: int, *, block: int = 0,
+              window: int = 0, slots: int | None = None, dtype=torch.bfloat16,
+              scale: float = 0.0) -> PbbDesc:
+    """Descriptor for a PBB ring (``block`` = B, ``slots`` = B) or, with ``window`` > 0, an SWA
+    ring (``slots`` >= ``window``, default ``window``)."""
+    if slots is None:
+        slots = window if window > 0 else block
+    code = {torch.float32: DTYPE_F32, torch.bfloat16: DTYPE_BF16}.get(dtype, dtype)
+    return PbbDesc(batch, n_q_heads, n_kv_heads, head_dim, block, window, slots, int(code),
+                   float(scale))
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+
+
+def _ptr(t: torch.Tensor | None):
+    return ctypes.c_void_p(0 if t is None else t.data_ptr())
+
+
+def _check(fn: str, status: int):
+    if status != PBB_OK:
+        raise PbbError(fn, status)
+
+
+def _expect(name: str, t: torch.Tensor, shape, dtype):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name}: expected a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name}: must be a GPU tensor, got {t.device}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name}: shape {tuple(t.shape)} != {tuple(shape)}")
+    if t.dtype != dtype:
+        raise ValueError(f"{name}: dtype {t.dtype} != {dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name}: must be contiguous")
+
+
+def ring_bytes(desc: PbbDesc) -> int:
+    out = ctypes.c_size_t()
+    _check("pbb_ring_bytes", load_library().pbb_ring_bytes(ctypes.byref(desc), ctypes.byref(out)))
+    return out.value
+
+
+def workspace_bytes(desc: PbbDesc) -> int:
+    out = ctypes.c_size_t()
+    _check("pbb_workspace_bytes",
+           load_library().pbb_workspace_bytes(ctypes.byref(desc), ctypes.byref(out)))
+    return out.value
+
+
+def swa_workspace_bytes(desc: PbbDesc) -> int:
+    out = ctypes.c_size_t()
+    _check("swa_workspace_bytes",
+           load_library().swa_workspace_bytes(ctypes.byref(desc), ctypes.byref(out)))
+    return out.value
+
+
+def ring_shape(desc: PbbDesc):
+    return (desc.batch, desc.n_kv_heads, desc.slots, desc.head_dim)
+
+
+def alloc_rings(desc: PbbDesc, device="cuda"):
+    """Allocate (uninitialised) K and V rings for ``desc``."""
+    shape = ring_shape(desc)
+    return (torch.empty(shape, dtype=desc.torch_dtype, device=device),
+            torch.empty(shape, dtype=desc.torch_dtype, device=device))
+
+
+def ring_init(desc: PbbDesc, k_ring: torch.Tensor, v_ring: torch.Tensor, stream=None):
+    for n, t in (("k_ring", k_ring), ("v_ring", v_ring)):
+        _expect(n, t, ring_shape(desc), desc.torch_dtype)
+    _check("pbb_ring_init", load_library().pbb_ring_init(
+        ctypes.byref(desc), _ptr(k_ring), _ptr(v_ring), _stream(stream)))
+
+
+def ring_fill(desc: PbbDesc, pos: torch.Tensor, k_src: torch.Tensor, v_src: torch.Tensor,
+              k_ring: torch.Tensor, v_ring: torch.Tensor, stream=None):
+    """Load history rows ``pos[b]-L .. pos[b]-1`` (``k_src`` [batch][Hkv][L][d]) into the rings."""
+    src_len = k_src.shape[2]
+    _expect("pos", pos, (desc.batch,), torch.int32)
+    for n, t in (("k_src", k_src), ("v_src", v_src)):
+        _expect(n, t, (desc.batch, desc.n_kv_heads, src_len, desc.head_dim), desc.torch_dtype)
+    for n, t in (("k_ring", k_ring), ("v_ring", v_ring)):
+        _expect(n, t, ring_shape(desc), desc.torch_dtype)
+    _check("pbb_ring_fill", load_library().pbb_ring_fill(
+        ctypes.byref(desc), _ptr(pos), _ptr(k_src), _ptr(v_src), int(src_len), _ptr(k_ring),
+        _ptr(v_ring), _stream(stream)))
+
+
+def _decode(fn: str, desc: PbbDesc, pos, q, k_new, v_new, k_ring, v_ring, out, workspace,
+            stream):
+    _expect("pos", pos, (desc.batch,), torch.int32)
+    _expect("q", q, (desc.batch, desc.n_q_heads, desc.head_dim), desc.torch_dtype)
+    _expect("out", out, (desc.batch, desc.n_q_heads, desc.head_dim), desc.torch_dtype)
+    for n, t in (("k_new", k_new), ("v_new", v_new)):
+        _expect(n, t, (desc.batch, desc.n_kv_heads, desc.head_dim), desc.torch_dtype)
+    for n, t in (("k_ring", k_ring), ("v_ring", v_ring)):
+        _expect(n, t, ring_shape(desc), desc.torch_dtype)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(fn, getattr(load_library(), fn)(
+        ctypes.byref(desc), _ptr(pos), _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(k_ring),
+        _ptr(v_ring), _ptr(out), _ptr(workspace), ctypes.c_size_t(ws_bytes), _stream(stream)))
+    return out
+
+
+def pbb_decode_step(desc: PbbDesc, pos, q, k_new, v_new, k_ring, v_ring, out, workspace=None,
+                    stream=None):
+    """Fused ring append + PBB attention for every sequence (see ``include/pbb.h``)."""
+    return _decode("pbb_decode_step", desc, pos, q, k_new, v_new, k_ring, v_ring, out, workspace,
+                   stream)
+
+
+def swa_decode_step(desc: PbbDesc, pos, q, k_new, v_new, k_ring, v_ring, out, workspace=None,
+                    stream=None):
+    """Fused ring append + sliding-window attention (baseline, same kernels)."""
+    return _decode("swa_decode_step", desc, pos, q, k_new, v_new, k_ring, v_ring, out, workspace,
+                   stream)
+
+
+def default_scale(head_dim: int) -> float:
+    return 1.0 / math.sqrt(head_dim)

@@ -1,0 +1,146 @@
+"""Decode-run harness shared by the GPU parity tests.
+
+Runs the HIP library through its C ABI on seeded inputs from :mod:`workloads` and compares
+against the CPU oracle on the same inputs.  The oracle reads absolute-position history that
+the generator produces independently of the ring.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+import numpy as np
+import torch
+
+import oracle
+import paper_2606_02680_amd as P
+import workloads as W
+
+
+def desc_for(cfg: W.Config, batch: int | None = None) -> P.PbbDesc:
+    dt = torch.float32 if cfg.dtype == "f32" else torch.bfloat16
+    b = cfg.batch if batch is None else batch
+    if cfg.mode == "swa":
+        return P.make_desc(b, cfg.hq, cfg.hkv, cfg.d, window=cfg.window, slots=cfg.slots, dtype=dt)
+    return P.make_desc(b, cfg.hq, cfg.hkv, cfg.d, block=cfg.block, dtype=dt)
+
+
+def bf16_tolerance_ok(got: np.ndarray, ref: np.ndarray):
+    """Elementwise |got - ref| <= 2e-2 + 2^-8 |ref| (2e-2 plus one bf16 rounding half-ulp)."""
+    return np.abs(got - ref) <= 2e-2 + np.abs(ref) * 2.0 ** -8
+
+
+def compare(cfg: W.Config, got: np.ndarray, ref: np.ndarray, what: str = ""):
+    """Assert the tolerance for the workload dtype; returns a metrics dict."""
+    got = got.astype(np.float64)
+    diff = np.abs(got - ref)
+    metrics = {"max_abs": float(diff.max()) if diff.size else 0.0}
+    if cfg.dtype == "f32":
+        assert metrics["max_abs"] <= 1e-5, f"{what}: fp32 max abs {metrics['max_abs']:.3e} > 1e-5"
+        return metrics
+    ok = bf16_tolerance_ok(got, ref)
+    if not ok.all():
+        idx = np.unravel_index(np.argmax(diff - (2e-2 + np.abs(ref) * 2.0 ** -8)), diff.shape)
+        raise AssertionError(f"{what}: bf16 tolerance violated at {idx}: got {got[idx]}, "
+                             f"ref {ref[idx]}")
+    g = got.reshape(-1, got.shape[-1])
+    r = ref.reshape(-1, ref.shape[-1])
+    rn = np.linalg.norm(r, axis=1)
+    rel = np.linalg.norm(g - r, axis=1) / np.maximum(rn, 1e-30)
+    cos = (g * r).sum(1) / np.maximum(np.linalg.norm(g, axis=1) * rn, 1e-30)
+    metrics["rel_l2_max"] = float(rel.max())
+    metrics["cos_min"] = float(cos.min())
+    assert metrics["rel_l2_max"] <= 1e-2, f"{what}: relative L2 {metrics['rel_l2_max']:.3e}"
+    assert metrics["cos_min"] >= 0.9998, f"{what}: cosine {metrics['cos_min']:.6f}"
+    return metrics
+
+
+def to_np(t: torch.Tensor) -> np.ndarray:
+    return t.detach().to("cpu", torch.float32).numpy()
+
+
+def bits(t: torch.Tensor) -> np.ndarray:
+    t = t.detach().cpu()
+    return (t.view(torch.int16) if t.dtype == torch.bfloat16 else t.view(torch.int32)).numpy()
+
+
+@dataclass
+class Run:
+    """A decode run of ``steps`` steps for the sequences of ``cfg`` starting at ``t0``."""
+    cfg: W.Config
+    t0: torch.Tensor                    # int64 [batch]
+    steps: int
+    device: torch.device
+    desc: P.PbbDesc = None
+    hist_len: int = 0                   # prefill window length (0: empty rings)
+    k_ring: torch.Tensor = None
+    v_ring: torch.Tensor = None
+    pos: torch.Tensor = None            # int32 [batch] on device
+    step_index: int = 0
+    metrics: list = field(default_factory=list)
+
+    def __post_init__(self):
+        self.desc = desc_for(self.cfg, batch=self.t0.numel())
+        self.k_ring, self.v_ring = P.alloc_rings(self.desc, self.device)
+        P.ring_init(self.desc, self.k_ring, self.v_ring)
+        self.pos = self.t0.to(torch.int32).to(self.device)
+        if self.cfg.prefill:
+            self.hist_len = self.desc.slots
+            ks = W.kv_window(self.cfg, "k", self.t0, self.hist_len, device=self.device)
+            vs = W.kv_window(self.cfg, "v", self.t0, self.hist_len, device=self.device)
+            P.ring_fill(self.desc, self.pos, ks, vs, self.k_ring, self.v_ring)
+            del ks, vs
+        self.seq = torch.arange(self.t0.numel(), dtype=torch.int64)
+
+    # ---- inputs -----------------------------------------------------------------------
+    def positions(self, i: int) -> torch.Tensor:
+        return self.t0 + i
+
+    def step_inputs(self, i: int):
+        p = self.positions(i)
+        q = W.q_at(self.cfg, p, device=self.device)
+        k = W.kv_at(self.cfg, "k", self.seq, p.view(-1, 1), device=self.device)[:, :, 0, :]
+        v = W.kv_at(self.cfg, "v", self.seq, p.view(-1, 1), device=self.device)[:, :, 0, :]
+        return q.contiguous(), k.contiguous(), v.contiguous()
+
+    def history(self, rows: np.ndarray, upto_step: int, back: int | None = None):
+        """History [n][Hkv][L][d] (workload dtype) for sequences ``rows`` covering positions
+        t0 - back .. t0 + upto_step (``back`` defaults to the pre-fill length), plus its first
+        position per sequence."""
+        back = self.hist_len if back is None else back
+        rows_t = torch.as_tensor(rows, dtype=torch.int64)
+        lo = self.t0[rows_t] - back
+        offs = torch.arange(0, back + upto_step + 1, dtype=torch.int64)
+        posm = lo.view(-1, 1) + offs.view(1, -1)
+        kh = W.kv_at(self.cfg, "k", rows_t, posm, device=self.device)
+        vh = W.kv_at(self.cfg, "v", rows_t, posm, device=self.device)
+        return kh, vh, lo.numpy()
+
+    # ---- one step ---------------------------------------------------------------------
+    def step(self, inputs=None):
+        q, k, v = self.step_inputs(self.step_index) if inputs is None else inputs
+        out = torch.empty_like(q)
+        fn = P.swa_decode_step if self.cfg.mode == "swa" else P.pbb_decode_step
+        fn(self.desc, self.pos, q, k, v, self.k_ring, self.v_ring, out)
+        self.pos += 1
+        self.step_index += 1
+        return q, out
+
+    def oracle_out(self, rows: np.ndarray, step: int, q: torch.Tensor, hist=None):
+        """fp64 oracle output [n][Hq][d] of step ``step`` for sequences ``rows``."""
+        kh, vh, lo = self.history(rows, step) if hist is None else hist
+        pos = (self.t0.numpy()[rows] + step).astype(np.int64)
+        mode = oracle.SWA if self.cfg.mode == "swa" else oracle.PBB
+        return oracle.decode(mode, pos, to_np(q[torch.as_tensor(rows, device=q.device)]), to_np(kh), to_np(vh), lo,
+                             block=self.cfg.block, window=self.cfg.window)
+
+    def expected_ring(self, rows: np.ndarray, step: int, which: str, hist=None):
+        """Bit pattern the ring must hold after ``step`` (0-based) has run."""
+        kh, vh, lo = self.history(rows, step) if hist is None else hist
+        h = kh if which == "k" else vh
+        t_last = self.t0.numpy()[rows] + step
+        first = np.maximum(0, self.t0.numpy()[rows] - self.hist_len)
+        return oracle.expected_ring(bits(h), lo, t_last, first, self.desc.slots)
+
+    def ring_rows(self, rows: np.ndarray, which: str) -> np.ndarray:
+        r = self.k_ring if which == "k" else self.v_ring
+        return bits(r[torch.as_tensor(rows, device=self.device)])

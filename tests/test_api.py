@@ -1,0 +1,156 @@
+"""C-ABI surface of libpbb.
+
+CPU tests: the library loads, exports every function ``include/pbb.h`` declares, and each
+invalid argument returns its documented status before anything is enqueued (fake, never
+dereferenced device addresses are enough for that).  GPU tests: a failing call leaves every
+buffer untouched, and the size queries agree with the paper's KV-bytes formula.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+import torch
+
+import paper_2606_02680_amd as P
+from paper_2606_02680_amd import pbb as B
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "pbb.h")
+A = 0x10000  # an aligned fake device address (never dereferenced: validation fails first)
+
+
+def _declared():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\S.*?\b((?:pbb|swa)_[a-z_]+)\s*\(", text, re.M)))
+
+
+def test_header_symbols_exported():
+    lib = B.load_library()
+    names = _declared()
+    assert set(names) == set(B.EXPORTS)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings():
+    for code in range(7):
+        assert B.lib_status_string(code).startswith(B.STATUS_NAMES[code])
+    assert "UNKNOWN" in B.lib_status_string(99)
+
+
+def _desc(**kw):
+    base = dict(batch=2, n_q_heads=8, n_kv_heads=2, head_dim=64, block=64, window=0, slots=64,
+                dtype=B.DTYPE_BF16, scale=0.0)
+    base.update(kw)
+    return B.PbbDesc(**base)
+
+
+def _decode(desc, fn="pbb_decode_step", **ptrs):
+    args = dict(pos=A, q=A, k_new=A, v_new=A, k_ring=A, v_ring=A, out=A, ws=0)
+    args.update(ptrs)
+    lib = B.load_library()
+    vp = ctypes.c_void_p
+    d = None if desc is None else ctypes.byref(desc)
+    return getattr(lib, fn)(d, vp(args["pos"]), vp(args["q"]), vp(args["k_new"]),
+                            vp(args["v_new"]), vp(args["k_ring"]), vp(args["v_ring"]),
+                            vp(args["out"]), vp(args["ws"]), ctypes.c_size_t(0), vp(0))
+
+
+@pytest.mark.parametrize("fn", ["pbb_decode_step", "swa_decode_step"])
+def test_null_arguments(fn):
+    desc = _desc(window=32, slots=64) if fn == "swa_decode_step" else _desc()
+    assert _decode(None, fn) == 1
+    for name in ("pos", "q", "k_new", "v_new", "k_ring", "v_ring", "out"):
+        assert _decode(desc, fn, **{name: 0}) == 1, name
+
+
+@pytest.mark.parametrize("bad", [
+    dict(batch=0), dict(n_kv_heads=0), dict(n_q_heads=6, n_kv_heads=4), dict(n_q_heads=34,
+    n_kv_heads=2), dict(head_dim=96), dict(head_dim=256), dict(block=63, slots=63),
+    dict(block=64, slots=128), dict(block=0, slots=0), dict(block=131072, slots=131072)])
+def test_pbb_shape_errors(bad):
+    assert _decode(_desc(**bad)) == 2
+
+
+@pytest.mark.parametrize("bad", [dict(window=65, slots=64), dict(window=-1, slots=64),
+                                 dict(window=8, slots=100000)])
+def test_swa_shape_errors(bad):
+    assert _decode(_desc(**bad), "swa_decode_step") == 2
+
+
+def test_swa_descriptor_rejected_by_pbb_step():
+    # slots != block under the PBB rules
+    assert _decode(_desc(window=64, slots=128, block=64)) == 2
+
+
+def test_dtype_error():
+    assert _decode(_desc(dtype=7)) == 3
+
+
+@pytest.mark.parametrize("name", ["q", "k_new", "v_new", "k_ring", "v_ring", "out"])
+def test_alignment_errors(name):
+    assert _decode(_desc(), **{name: A + 8}) == 4
+    assert _decode(_desc(window=64, slots=64), "swa_decode_step", **{name: A + 2}) == 4
+
+
+def test_pos_alignment():
+    assert _decode(_desc(), pos=A + 2) == 4
+
+
+def test_ring_bytes_and_workspace():
+    desc = _desc()
+    assert P.ring_bytes(desc) == 2 * 2 * 64 * 64 * 2
+    assert P.workspace_bytes(desc) == 0
+    swa = _desc(window=48, slots=64)
+    assert P.ring_bytes(swa) == 2 * 2 * 64 * 64 * 2
+    assert P.swa_workspace_bytes(swa) == 0
+    # Paper's local KV storage 2*batch*b*H_KV*d_h*u = 65,536 B at (1, 128, 2, 64, bf16)
+    paper = P.make_desc(1, 12, 2, 64, block=128)
+    assert 2 * P.ring_bytes(paper) == 65536
+    with pytest.raises(P.PbbError):
+        P.ring_bytes(_desc(head_dim=80))
+
+
+def test_ring_fill_and_init_errors():
+    lib = B.load_library()
+    vp = ctypes.c_void_p
+    desc = _desc()
+    assert lib.pbb_ring_init(None, vp(A), vp(A), vp(0)) == 1
+    assert lib.pbb_ring_init(ctypes.byref(desc), vp(0), vp(A), vp(0)) == 1
+    assert lib.pbb_ring_init(ctypes.byref(desc), vp(A + 4), vp(A), vp(0)) == 4
+    fill = lambda n, **kw: lib.pbb_ring_fill(ctypes.byref(desc), vp(kw.get("pos", A)),
+                                             vp(kw.get("ks", A)), vp(A), n, vp(A), vp(A), vp(0))
+    assert fill(65) == 2          # longer than the ring
+    assert fill(-1) == 2
+    assert fill(8, ks=0) == 1
+    assert fill(8, pos=0) == 1
+    assert fill(8, ks=A + 8) == 4
+
+
+# ---------------------------------------------------------------------------------------
+# GPU: failing calls write nothing
+
+@pytest.mark.gpu
+def test_failed_calls_leave_buffers_untouched(cuda):
+    desc = P.make_desc(2, 8, 2, 64, block=64)
+    canary = 0x5A5A
+    mk = lambda *s: torch.full(s, canary, dtype=torch.int16, device=cuda).view(torch.bfloat16)
+    q, out = mk(2, 8, 64), mk(2, 8, 64)
+    kn, vn = mk(2, 2, 64), mk(2, 2, 64)
+    kr, vr = mk(2, 2, 64, 64), mk(2, 2, 64, 64)
+    pos = torch.zeros(2, dtype=torch.int32, device=cuda)
+    bad = P.make_desc(2, 8, 3, 64, block=64)  # 8 % 3 != 0
+    ptr = lambda t: t.data_ptr()
+    st = _decode(bad, pos=ptr(pos), q=ptr(q), k_new=ptr(kn), v_new=ptr(vn), k_ring=ptr(kr),
+                 v_ring=ptr(vr), out=ptr(out))
+    assert st == 2
+    st = _decode(desc, pos=ptr(pos), q=ptr(q) + 2, k_new=ptr(kn), v_new=ptr(vn),
+                 k_ring=ptr(kr), v_ring=ptr(vr), out=ptr(out))
+    assert st == 4
+    torch.cuda.synchronize()
+    for t in (q, out, kn, vn, kr, vr):
+        assert bool((t.view(torch.int16) == canary).all())
+    # A valid call on the same buffers does write (sanity of the canary check).
+    P.pbb_decode_step(desc, pos, q.zero_(), kn.zero_(), vn.zero_(), kr.zero_(), vr.zero_(), out)
+    torch.cuda.synchronize()
+    assert not bool((out.view(torch.int16) == canary).any())

@@ -1,0 +1,219 @@
+"""GPU parity: the HIP library (through its C ABI) against the fp64 CPU oracle.
+
+Outputs: fp32 within max-abs 1e-5; bf16 within |d| <= 2e-2 + 2^-8 |ref| elementwise plus
+relative L2 <= 1e-2 and cosine >= 0.9998 per (sequence, head).  Rings: bit-exact against the
+oracle's ring image (slot = position mod slots, Appendix F.1).
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as W
+from tests.harness import Run, bits, compare, to_np
+
+pytestmark = pytest.mark.gpu
+
+
+def _lockstep(cfg, device, check_out, check_ring, batch=None):
+    """Run cfg from position 0 (or cfg's t0) for cfg.steps steps, checking selected steps."""
+    b = cfg.batch if batch is None else batch
+    t0 = W.initial_positions(cfg.with_(batch=b))
+    run = Run(cfg, t0, cfg.steps, device)
+    rows = np.arange(b)
+    hist = run.history(rows, cfg.steps - 1)
+    print(f"[lockstep] {cfg.name} batch={b} steps={cfg.steps}", flush=True)
+    worst = 0.0
+    for i in range(cfg.steps):
+        q, out = run.step()
+        if check_out(i):
+            ref = run.oracle_out(rows, i, q, hist=hist)
+            m = compare(cfg, to_np(out), ref, what=f"{cfg.name} step {i}")
+            worst = max(worst, m["max_abs"])
+        if check_ring(i):
+            for which in ("k", "v"):
+                exp = run.expected_ring(rows, i, which, hist=hist)
+                got = run.ring_rows(rows, which)
+                assert np.array_equal(got, exp), f"{cfg.name} ring {which} mismatch after step {i}"
+    return worst
+
+
+def test_c1_tiny_fp32_every_step(cuda):
+    cfg = W.get_config("c1")
+    worst = _lockstep(cfg, cuda, check_out=lambda i: True, check_ring=lambda i: True)
+    print(f"c1 worst max-abs {worst:.3e}")
+
+
+def test_c2_lockstep_bf16(cuda):
+    """2048 steps from 0 with B = 512: outputs every third step (3 is coprime to 512, so
+    every phase r is checked), rings around every boundary and half-boundary."""
+    cfg = W.get_config("c2")
+    h = cfg.block // 2
+    special = {0, 1, h - 1, h, h + 1, cfg.block - 1}
+    worst = _lockstep(cfg, cuda, check_out=lambda i: i % 3 == 0 or (i % cfg.block) in special,
+                      check_ring=lambda i: (i % h) in (0, 1, h - 1) or i == cfg.steps - 1)
+    print(f"c2 worst max-abs {worst:.3e}")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("d,hq,hkv,block", [(64, 1, 1, 2), (128, 2, 1, 4), (64, 16, 1, 16),
+                                            (128, 8, 2, 32), (64, 6, 3, 8), (128, 16, 2, 64)])
+def test_small_shapes_every_step(cuda, dtype, d, hq, hkv, block):
+    """Group sizes 1..16, both head dims, tiny blocks (one to several 32-key tiles, ragged
+    tails), every step over five blocks, ring checked every step."""
+    cfg = W.Config(f"small-{dtype}-{d}-{hq}-{hkv}-{block}", "pbb", batch=3, hq=hq, hkv=hkv,
+                   d=d, block=block, slots=block, window=0, dtype=dtype, seed=5,
+                   value_scale=1.0, pos_hi=0, steps=5 * block + 3)
+    _lockstep(cfg, cuda, check_out=lambda i: True, check_ring=lambda i: True)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("window,slots", [(48, 64), (64, 64), (37, 40), (1, 1), (100, 160)])
+def test_swa_small_every_step(cuda, dtype, window, slots):
+    cfg = W.Config(f"swa-{dtype}-{window}-{slots}", "swa", batch=2, hq=4, hkv=2, d=64,
+                   block=0, slots=slots, window=window, dtype=dtype, seed=6, value_scale=1.0,
+                   pos_hi=0, steps=3 * slots + 5)
+    _lockstep(cfg, cuda, check_out=lambda i: True, check_ring=lambda i: True)
+
+
+def _edge_positions(cfg, n):
+    """Initial positions covering the degenerate phases of a block of size B (or a window)."""
+    B = cfg.block if cfg.mode == "pbb" else cfg.slots
+    h = B // 2
+    k = 37  # an arbitrary later block
+    edges = [0, 1, h - 1, h, B - 1, B, B + 1, B + h - 1, B + h, k * B, k * B + 1,
+             k * B + h - 1, k * B + h, k * B + B - 1, cfg.pos_hi - 1]
+    return [e for e in edges if 0 <= e][:n]
+
+
+def _sampled(cfg, device, steps, n_rows=24, seed=0):
+    """Full-size batch with forced edge positions; checks sampled sequences at every step."""
+    t0 = W.initial_positions(cfg)
+    edges = _edge_positions(cfg, n_rows // 2)
+    t0[:len(edges)] = torch.tensor(edges, dtype=torch.int64)
+    print(f"[sampled] {cfg.name} batch={cfg.batch} steps={steps}", flush=True)
+    run = Run(cfg, t0, steps, device)
+    rng = np.random.default_rng(seed)
+    rest = rng.choice(np.arange(len(edges), cfg.batch), size=n_rows - len(edges), replace=False)
+    rows = np.concatenate([np.arange(len(edges)), np.sort(rest)])
+    hist = run.history(rows, steps - 1)
+    worst = {}
+    for i in range(steps):
+        q, out = run.step()
+        ref = run.oracle_out(rows, i, q, hist=hist)
+        got = to_np(out[torch.as_tensor(rows, device=device)])
+        m = compare(cfg, got, ref, what=f"{cfg.name} step {i}")
+        worst = {k: max(worst.get(k, -1e30), v) if k != "cos_min" else min(worst.get(k, 1e30), v)
+                 for k, v in m.items()}
+    for which in ("k", "v"):
+        exp = run.expected_ring(rows, steps - 1, which, hist=hist)
+        assert np.array_equal(run.ring_rows(rows, which), exp), f"{cfg.name} ring {which}"
+    return run, rows, hist, worst
+
+
+def test_c3_sampled_full_batch(cuda):
+    cfg = W.get_config("c3")
+    _, _, _, worst = _sampled(cfg, cuda, steps=3)
+    print(f"c3 {worst}")
+
+
+def test_c4_ragged_spiked_sampled(cuda):
+    cfg = W.get_config("c4")
+    _, _, _, worst = _sampled(cfg, cuda, steps=3, n_rows=32)
+    print(f"c4 {worst}")
+
+
+def test_c5_swa_sampled(cuda):
+    cfg = W.get_config("c5")
+    _, _, _, worst = _sampled(cfg, cuda, steps=2, n_rows=16)
+    print(f"c5 {worst}")
+
+
+def _support_variant(kind, t, B):
+    h = B // 2
+    p, r = B * (t // B), t % B
+    if kind == "no_bridge":
+        return list(range(p, t + 1))
+    if kind == "bridge_always":
+        return list(range(max(0, p - h), t + 1))
+    if kind == "start_off_by_one":
+        lo = max(0, h * (t // h - 1))
+        return list(range(max(0, lo + (1 if lo > 0 else 0)), t + 1))
+    if kind == "swa_w_eq_b":
+        return list(range(max(0, t - B + 1), t + 1))
+    raise ValueError(kind)
+
+
+def test_wrong_support_controls_are_detected(cuda):
+    """The tolerance can see support mistakes: at c2's scale (N(0,1)/8, where an all-zero
+    output would pass a plain 2e-2 max-abs bound), outputs computed on plausible wrong
+    supports or a strided GQA mapping fail the same comparison the GPU output passes."""
+    cfg = W.get_config("c2").with_(batch=4, steps=1)
+    B, h = cfg.block, cfg.block // 2
+    run_t0 = torch.tensor([B + 3, 3 * B + h + 5, 2 * B + 7, B + 1], dtype=torch.int64)
+    run = Run(cfg.with_(prefill=True), run_t0, 1, cuda)
+    rows = np.arange(4)
+    hist = run.history(rows, 0, back=2 * B)
+    q, out = run.step()
+    ref = run.oracle_out(rows, 0, q, hist=hist)
+    compare(cfg, to_np(out), ref, what="gpu vs oracle")
+    kh, vh, lo = (to_np(hist[0]), to_np(hist[1]), hist[2])
+    qn = to_np(q)
+    G = cfg.group
+    for kind in ("no_bridge", "bridge_always", "start_off_by_one", "swa_w_eq_b", "gqa_strided"):
+        wrong = np.zeros_like(ref)
+        for b in range(4):
+            t = int(run_t0[b])
+            if kind == "gqa_strided":
+                sup = oracle.pbb_support(t, B)
+            else:
+                sup = _support_variant(kind, t, B)
+            idx = np.array(sup) - lo[b]
+            for i in range(cfg.hq):
+                g = (i % cfg.hkv) if kind == "gqa_strided" else i // G
+                wrong[b, i], _ = oracle.attend(qn[b, i], kh[b, g, idx], vh[b, g, idx])
+        with pytest.raises(AssertionError):
+            compare(cfg, to_np(out), wrong, what=kind)
+    with pytest.raises(AssertionError):
+        compare(cfg, np.zeros_like(ref), ref, what="all zeros")
+
+
+def test_negative_position_is_inert(cuda):
+    cfg = W.get_config("c2").with_(batch=2, steps=1)
+    run = Run(cfg, torch.tensor([5, 7]), 1, cuda)
+    run.pos[1] = -1
+    before = bits(run.k_ring[1]).copy()
+    q, out = run.step()
+    assert not to_np(out[1]).any()
+    assert np.array_equal(bits(run.k_ring[1]), before)
+
+
+def test_repeat_is_bitwise_deterministic(cuda):
+    cfg = W.get_config("c4").with_(batch=64)
+    t0 = W.initial_positions(cfg)
+    a = Run(cfg, t0, 1, cuda)
+    b = Run(cfg, t0, 1, cuda)
+    inputs = a.step_inputs(0)
+    _, oa = a.step(inputs)
+    _, ob = b.step(inputs)
+    assert torch.equal(oa.view(torch.int16), ob.view(torch.int16))
+    assert torch.equal(a.k_ring.view(torch.int16), b.k_ring.view(torch.int16))
+
+
+def test_snapshot_restore_continues_bitwise(cuda):
+    """Ring + positions are the whole decode state: restoring a snapshot and continuing
+    reproduces an uninterrupted run bit for bit."""
+    cfg = W.get_config("c2").with_(batch=8)
+    t0 = W.initial_positions(cfg)
+    run = Run(cfg, t0, 0, cuda)
+    for _ in range(300):
+        run.step()
+    snap = (run.k_ring.clone(), run.v_ring.clone(), run.pos.clone(), run.step_index)
+    outs_a = [run.step()[1].clone() for _ in range(300)]
+    run.k_ring.copy_(snap[0]); run.v_ring.copy_(snap[1]); run.pos.copy_(snap[2])
+    run.step_index = snap[3]
+    outs_b = [run.step()[1].clone() for _ in range(300)]
+    for x, y in zip(outs_a, outs_b):
+        assert torch.equal(x.view(torch.int16), y.view(torch.int16))
