@@ -1,0 +1,301 @@
+#!/usr/bin/env python3
+"""Benchmark: PBB decode attention-core throughput on one MI355X.
+
+One step = one fused ring-append + PBB-attention launch (``pbb_decode_step``) for every
+sequence of the batch, followed by the position advance ``pos += 1`` on the same stream.
+Inputs are seeded synthetic tensors already resident in HBM; rings are pre-filled.
+
+Default workload (c3): batch 256, Hq 32, Hkv 8, head_dim 128, B 2048, bf16, positions
+uniform in [0, 512K).  Also reported: the same-library sliding-window ring on the same
+tensors (W = 2B = 4096 in 4096 slots, plus the paper-matched W = B), and the ragged GQA-8
+workload (c4).
+
+Prints ONE JSON line.  Roofline: algorithmic bytes of the support actually read (ring K and
+V rows of |A(t)| - 1 sources, q, out, the new K/V and their slot write, pos) divided by the
+decode kernel's mean duration from HIP events on the launch stream, against 8 TB/s.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+HBM_PEAK_GBPS = 8000.0
+ROOT = os.path.dirname(os.path.abspath(__file__))
+METRIC = "PBB decode attention-core tokens/s + achieved HBM GB/s (% of peak), 1 GPU"
+
+
+def support_size(t, cfg):
+    """|A(t)| for each position (PBB: t - a(t) + 1 with a(t) = max(0, h(floor(t/h) - 1));
+    SWA: min(t + 1, W))."""
+    import torch
+    if cfg.mode == "swa":
+        return torch.clamp(t + 1, max=cfg.window)
+    h = cfg.block // 2
+    a = torch.clamp(h * (torch.div(t, h, rounding_mode="floor") - 1), min=0)
+    return t - a + 1
+
+
+def step_bytes(t, cfg):
+    """Algorithmic HBM bytes of one decode step for positions ``t`` (int64 [batch])."""
+    u = 4 if cfg.dtype == "f32" else 2
+    n = support_size(t, cfg) - 1
+    per_seq = n * 2 * cfg.hkv * cfg.d * u + 2 * cfg.hq * cfg.d * u + 4 * cfg.hkv * cfg.d * u + 4
+    return int(per_seq.sum())
+
+
+def _kernel_hash():
+    h = hashlib.sha256()
+    for f in ("pbb_kernels.hip", "pbb_api.cpp", "pbb_internal.h"):
+        with open(os.path.join(ROOT, "paper_2606_02680_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def _traffic_from_profile(workload_key):
+    """HBM traffic per launch from the committed rocprofv3 counter summary, or None when the
+    kernel sources changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", f"decode_bf16_{workload_key}_counters.txt")
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    with open(path) as f:
+        for ln in f:
+            if ":" in ln:
+                k, v = ln.split(":", 1)
+                vals[k.strip()] = v.strip()
+    if vals.get("kernel_source_hash") != _kernel_hash():
+        return None
+    try:
+        return float(vals["hbm_bytes_per_launch_scaled"])
+    except (KeyError, ValueError):
+        return None
+
+
+class Workload:
+    """Rings + pre-generated per-step inputs for one config, resident on the GPU."""
+
+    def __init__(self, cfg, t0, n_steps, device, inputs=None):
+        import torch
+        import paper_2606_02680_amd as P
+        import workloads as W
+        self.cfg, self.t0, self.device = cfg, t0, device
+        dt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+        if cfg.mode == "swa":
+            self.desc = P.make_desc(cfg.batch, cfg.hq, cfg.hkv, cfg.d, window=cfg.window,
+                                    slots=cfg.slots, dtype=dt)
+            self.fn = P.swa_decode_step
+        else:
+            self.desc = P.make_desc(cfg.batch, cfg.hq, cfg.hkv, cfg.d, block=cfg.block, dtype=dt)
+            self.fn = P.pbb_decode_step
+        self.k_ring, self.v_ring = P.alloc_rings(self.desc, device)
+        P.ring_init(self.desc, self.k_ring, self.v_ring)
+        self.pos0 = t0.to(torch.int32).to(device)
+        self.pos = self.pos0.clone()
+        L = self.desc.slots
+        ks = W.kv_window(cfg, "k", t0, L, device=device)
+        vs = W.kv_window(cfg, "v", t0, L, device=device)
+        P.ring_fill(self.desc, self.pos, ks, vs, self.k_ring, self.v_ring)
+        del ks, vs
+        if inputs is None:
+            inputs = (W.q_steps(cfg, t0, 0, n_steps, device=device),
+                      W.kv_steps(cfg, "k", t0, 0, n_steps, device=device),
+                      W.kv_steps(cfg, "v", t0, 0, n_steps, device=device))
+        self.inputs = inputs
+        self.out = torch.empty_like(inputs[0][0])
+        torch.cuda.synchronize()
+
+    def step(self, i):
+        q, k, v = self.inputs[0][i], self.inputs[1][i], self.inputs[2][i]
+        self.fn(self.desc, self.pos, q, k, v, self.k_ring, self.v_ring, self.out)
+
+    def timed(self, warmup, steps):
+        """Returns (elapsed seconds of the whole loop, mean kernel seconds, algorithmic bytes)."""
+        import torch
+        for i in range(warmup):
+            self.step(i)
+            self.pos += 1
+        torch.cuda.synchronize()
+        starts = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+        ends = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+        total_bytes = 0
+        t_first = (self.t0 + warmup)
+        for i in range(steps):
+            total_bytes += step_bytes(t_first + i, self.cfg)
+        torch.cuda.synchronize()
+        w0 = time.perf_counter()
+        for i in range(steps):
+            starts[i].record()
+            self.step(warmup + i)
+            ends[i].record()
+            self.pos += 1
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - w0
+        kern = sum(s.elapsed_time(e) for s, e in zip(starts, ends)) / 1e3 / steps
+        return elapsed, kern, total_bytes
+
+
+def cpu_baseline(cfg, t0, device, budget_s=12.0):
+    """Time the fp64 CPU oracle on the first decode step of the workload's first sequences,
+    repeating the sample until ``budget_s`` seconds have elapsed."""
+    import numpy as np
+    import torch
+    import oracle
+    import workloads as W
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or (os.cpu_count() or 1)
+    n = min(32, cfg.batch)
+    rows = torch.arange(n, dtype=torch.int64)
+    back = cfg.slots
+    lo = t0[:n] - back
+    posm = lo.view(-1, 1) + torch.arange(0, back + 1, dtype=torch.int64).view(1, -1)
+    kh = W.kv_at(cfg, "k", rows, posm, device=device).float().cpu().numpy()
+    vh = W.kv_at(cfg, "v", rows, posm, device=device).float().cpu().numpy()
+    q = W.q_at(cfg, t0[:n], device=device).float().cpu().numpy()
+    mode = oracle.SWA if cfg.mode == "swa" else oracle.PBB
+    pos = t0[:n].numpy().astype(np.int64)
+    oracle.decode(mode, pos[:1], q[:1], kh[:1], vh[:1], lo[:1].numpy(), block=cfg.block,
+                  window=cfg.window, n_threads=1)  # load the library outside the clock
+    done, w0 = 0, time.perf_counter()
+    while True:
+        oracle.decode(mode, pos, q, kh, vh, lo.numpy(), block=cfg.block, window=cfg.window,
+                      n_threads=threads)
+        done += n
+        if time.perf_counter() - w0 >= budget_s:
+            break
+    el = time.perf_counter() - w0
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            model = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), "")
+    except OSError:
+        pass
+    return {"value": done / el, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"first decode step of sequences 0..{n - 1} of {cfg.name} (all {cfg.hq} "
+                      f"query heads each), repeated {done // n}x over {el:.1f} s; fp64 C oracle, "
+                      f"{threads} threads; host CPU: {model}"}
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=1000)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", default="c3", choices=["c3", "c4", "c5"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the SWA-ring and ragged-batch comparison runs")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="only time a plain 1 GiB device copy (HBM counter calibration)")
+    args = ap.parse_args(argv)
+    if args.gpus != 1:
+        print(f"bench.py: this build measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the decode core shards by sequence or KV head with no exchange; see DESIGN.md)",
+              file=sys.stderr)
+        return 2
+
+    import torch
+    import workloads as W
+    sys.path.insert(0, ROOT)
+    import paper_2606_02680_amd as P
+    P.load_library()
+    device = torch.device("cuda:0")
+    torch.cuda.set_device(device)
+
+    if args.copy_probe:
+        n = 1 << 29  # 1 GiB of bf16
+        x = torch.ones(n, dtype=torch.bfloat16, device=device)
+        y = torch.empty_like(x)
+        y.copy_(x)
+        torch.cuda.synchronize()
+        w0 = time.perf_counter()
+        for _ in range(5):
+            y.copy_(x)
+        torch.cuda.synchronize()
+        el = (time.perf_counter() - w0) / 5
+        print(json.dumps({"copy_probe_bytes_read": 2 * n, "copy_probe_bytes_written": 2 * n,
+                          "copy_probe_gbps_read_plus_write": 4 * n / el / 1e9}), flush=True)
+        return 0
+
+    cfg = W.get_config(args.config)
+    n_steps = args.warmup + args.steps
+    t0 = W.initial_positions(cfg)
+    print(f"[bench] preparing {cfg.name} ({n_steps} steps of inputs)", file=sys.stderr, flush=True)
+    wl = Workload(cfg, t0, n_steps, device)
+    elapsed, kern_s, total_bytes = wl.timed(args.warmup, args.steps)
+    tokens = cfg.batch * args.steps
+    value = tokens / elapsed
+    achieved = total_bytes / args.steps / kern_s / 1e9
+    result = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": elapsed / args.steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: batch {cfg.batch}, Hq {cfg.hq}, Hkv {cfg.hkv}, "
+                               f"head_dim {cfg.d}, B {cfg.block}, ring {cfg.slots} slots, "
+                               f"positions U[0,{cfg.pos_hi}), pre-filled rings",
+                   "batch": cfg.batch, "n_q_heads": cfg.hq, "n_kv_heads": cfg.hkv,
+                   "head_dim": cfg.d, "block": cfg.block, "slots": cfg.slots,
+                   "window": cfg.window, "parallelism": "single GPU"},
+        "hbm_gbps_step": total_bytes / elapsed / 1e9,
+        "bytes_per_token": total_bytes / tokens,
+        "kernel_us": kern_s * 1e6,
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS,
+                     "traffic": _traffic_from_profile(args.config)},
+    }
+    print(f"[bench] {cfg.name}: {value:.4g} tokens/s, kernel {kern_s * 1e6:.1f} us, "
+          f"{achieved:.1f} GB/s", file=sys.stderr, flush=True)
+
+    if not args.no_extras and args.config == "c3":
+        extra = {}
+        ext_steps = min(args.steps, 200)
+        inputs = wl.inputs
+        del wl
+        torch.cuda.empty_cache()
+        for name, c in (("swa_ring_w4096_s4096", W.get_config("c5")),
+                        ("swa_ring_w2048_s2048", W.get_config("c5").with_(window=2048,
+                                                                          slots=2048))):
+            sw = Workload(c, t0, n_steps, device, inputs=inputs)
+            el, ks, tb = sw.timed(args.warmup, ext_steps)
+            extra[name] = {"tokens_per_s": cfg.batch * ext_steps / el, "kernel_us": ks * 1e6,
+                           "bytes_per_token": tb / (cfg.batch * ext_steps),
+                           "hbm_gbps_kernel": tb / ext_steps / ks / 1e9,
+                           "pbb_over_swa_tokens_per_s": value / (cfg.batch * ext_steps / el)}
+            del sw
+            torch.cuda.empty_cache()
+        del inputs
+        torch.cuda.empty_cache()
+        c4 = W.get_config("c4")
+        t4 = W.initial_positions(c4)
+        w4 = Workload(c4, t4, args.warmup + ext_steps, device)
+        el, ks, tb = w4.timed(args.warmup, ext_steps)
+        extra["c4_ragged_gqa8"] = {"tokens_per_s": c4.batch * ext_steps / el,
+                                   "kernel_us": ks * 1e6,
+                                   "bytes_per_token": tb / (c4.batch * ext_steps),
+                                   "hbm_gbps_kernel": tb / ext_steps / ks / 1e9,
+                                   "frac_of_peak": tb / ext_steps / ks / 1e9 / HBM_PEAK_GBPS}
+        del w4
+        result["extra"] = extra
+        result["paper_context"] = ("Flash-PBB 1.82x Flash-SWA decode-core throughput on an RTX "
+                                   "4090 (48 GB), BF16, batch 1, Hkv 2, d 64, b 128 vs w 128")
+
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
+        result["cpu_baseline"] = cpu_baseline(cfg, t0, device)
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -75,6 +75,28 @@ def spike_mask(cfg, seq: torch.Tensor, pos: torch.Tensor) -> torch.Tensor:
     return h < int(cfg.spike_prob * 4294967296.0)
 
 
+def _normal_block(cfg, stream: int, seq: torch.Tensor, heads: int, pos: torch.Tensor, device,
+                  spike: bool, chunk: int) -> torch.Tensor:
+    """N(0,1)*value_scale values [n_seq][heads][n_pos][d] (workload dtype) for sequences
+    ``seq`` and absolute positions ``pos`` [n_seq][n_pos]; negative positions give zeros."""
+    n_seq, n_pos = pos.shape
+    out = torch.empty((n_seq, heads, n_pos, cfg.d), dtype=_dtype(cfg.dtype), device=device)
+    per = max(1, chunk // max(1, heads * n_pos * cfg.d))
+    for i in range(0, n_seq, per):
+        sq = seq[i:i + per].to(device)
+        ps = pos[i:i + per].to(device)
+        valid = ps >= 0
+        ctr = _counter(sq, heads, ps.clamp(min=0), cfg.d, device)
+        x = hash_normal(ctr, cfg.seed, stream) * cfg.value_scale
+        if spike and cfg.spike_prob > 0.0:
+            m = spike_mask(cfg, sq, ps.clamp(min=0))
+            x = torch.where(m.unsqueeze(1).unsqueeze(-1), x * cfg.spike_scale, x)
+        x = torch.where(valid.unsqueeze(1).unsqueeze(-1), x, torch.zeros((), dtype=x.dtype,
+                                                                          device=x.device))
+        out[i:i + per] = x.to(out.dtype)
+    return out
+
+
 def kv_at(cfg, which: str, seq: torch.Tensor, pos: torch.Tensor, device="cpu",
           chunk: int = 1 << 24) -> torch.Tensor:
     """Keys (``which='k'``) or values (``'v'``) at absolute positions.
@@ -85,22 +107,25 @@ def kv_at(cfg, which: str, seq: torch.Tensor, pos: torch.Tensor, device="cpu",
     stream = {"k": STREAM_K, "v": STREAM_V}[which]
     seq = torch.as_tensor(seq, dtype=torch.int64).view(-1)
     pos = torch.as_tensor(pos, dtype=torch.int64).view(seq.numel(), -1)
-    n_seq, n_pos = pos.shape
-    out = torch.empty((n_seq, cfg.hkv, n_pos, cfg.d), dtype=_dtype(cfg.dtype), device=device)
-    per = max(1, chunk // max(1, cfg.hkv * n_pos * cfg.d))
-    for i in range(0, n_seq, per):
-        sq = seq[i:i + per].to(device)
-        ps = pos[i:i + per].to(device)
-        valid = ps >= 0
-        ctr = _counter(sq, cfg.hkv, ps.clamp(min=0), cfg.d, device)
-        x = hash_normal(ctr, cfg.seed, stream) * cfg.value_scale
-        if cfg.spike_prob > 0.0:
-            m = spike_mask(cfg, sq, ps.clamp(min=0))
-            x = torch.where(m.unsqueeze(1).unsqueeze(-1), x * cfg.spike_scale, x)
-        x = torch.where(valid.unsqueeze(1).unsqueeze(-1), x, torch.zeros((), dtype=x.dtype,
-                                                                          device=x.device))
-        out[i:i + per] = x.to(out.dtype)
-    return out
+    return _normal_block(cfg, stream, seq, cfg.hkv, pos, device, True, chunk)
+
+
+def kv_steps(cfg, which: str, t0: torch.Tensor, first: int, n: int, device="cpu") -> torch.Tensor:
+    """New keys/values of ``n`` consecutive decode steps: [n][batch][Hkv][d], step ``i``
+    holding position ``t0[b] + first + i``."""
+    t0 = torch.as_tensor(t0, dtype=torch.int64).view(-1)
+    pos = t0.view(-1, 1) + first + torch.arange(n, dtype=torch.int64).view(1, -1)
+    x = kv_at(cfg, which, torch.arange(t0.numel(), dtype=torch.int64), pos, device=device)
+    return x.permute(2, 0, 1, 3).contiguous()
+
+
+def q_steps(cfg, t0: torch.Tensor, first: int, n: int, device="cpu") -> torch.Tensor:
+    """Queries of ``n`` consecutive decode steps: [n][batch][Hq][d]."""
+    t0 = torch.as_tensor(t0, dtype=torch.int64).view(-1)
+    pos = t0.view(-1, 1) + first + torch.arange(n, dtype=torch.int64).view(1, -1)
+    seq = torch.arange(t0.numel(), dtype=torch.int64)
+    x = _normal_block(cfg, STREAM_Q, seq, cfg.hq, pos, device, False, 1 << 24)
+    return x.permute(2, 0, 1, 3).contiguous()
 
 
 def kv_window(cfg, which: str, t0: torch.Tensor, length: int, device="cpu") -> torch.Tensor:
@@ -117,9 +142,8 @@ def q_at(cfg, pos: torch.Tensor, device="cpu") -> torch.Tensor:
     """Queries [batch][Hq][d] of every sequence decoding absolute position ``pos[b]``."""
     pos = torch.as_tensor(pos, dtype=torch.int64).view(-1)
     seq = torch.arange(pos.numel(), dtype=torch.int64)
-    ctr = _counter(seq.to(device), cfg.hq, pos.to(device).view(-1, 1), cfg.d, device)
-    x = hash_normal(ctr, cfg.seed, STREAM_Q) * cfg.value_scale
-    return x[:, :, 0, :].to(_dtype(cfg.dtype)).contiguous()
+    x = _normal_block(cfg, STREAM_Q, seq, cfg.hq, pos.view(-1, 1), device, False, 1 << 24)
+    return x[:, :, 0, :].contiguous()
 
 
 def initial_positions(cfg) -> torch.Tensor:
