@@ -275,18 +275,30 @@ __global__ __launch_bounds__(256) void decode_f32_kernel(DecodeArgs a) {
 //           16+4j..16+4j+3; the running maximum is shared across the four quarters.
 //   values  O^T[16 channels][16 heads] += V^T P^T.  P^T's B operand is exactly the score
 //           registers (rounded to bf16), so the key order of the contraction is fixed by
-//           the score layout; V is staged in a wave-private LDS tile and read transposed.
-// Padded heads (h >= G) compute on zero queries and are never stored.  Wave results are
-// merged through LDS with Eq.(lse) (Appendix A.4) and written as bf16 (RNE).
+//           the score layout.  V rows go from HBM straight into a double-buffered,
+//           wave-private LDS tile (global_load_lds_dwordx4: no registers) and are read back
+//           transposed, one bf16 per lane and row.
+// The next step's K registers and V tile are in flight while the current step computes.
+// Every step issues the same number of loads (keys past the end read the current token's
+// row and are masked out of the softmax), so one vmcnt wait orders the LDS reads after the
+// tile's DMA.  Padded heads (h >= G) compute on zero queries and are never stored.  Wave
+// results are merged through LDS with Eq.(lse) (Appendix A.4) and written as bf16 (RNE).
+//
+// V tile layout: the 32 rows of a step form 32/RPI groups of RPI rows, one group per 1 KiB
+// DMA (lane l lands at byte 16 l).  Group pitch and, for D = 64, a 16-byte piece swizzle in
+// the upper row quad make the transposed reads of rows 4j+e (j = 0..3) hit 32 distinct banks.
 template <int D, int NW>
-__global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
-  constexpr int KK = D / 32;          // 32-channel slices of the score contraction
-  constexpr int NB = D / 16;          // 16-channel blocks of the output
-  constexpr int ROWB = D * 2 + 16;    // LDS pitch of one staged V row (bytes, padded)
-  constexpr int PPR = D / 8;          // 16-byte pieces per V row
-  constexpr int RPI = 64 / PPR;       // V rows covered by one 16-byte load of the wave
-  constexpr int VLD = 32 / RPI;       // 16-byte V loads per lane per step
-  constexpr int STAGE_BYTES = NW * 32 * ROWB;
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) void decode_bf16_kernel(DecodeArgs a) {
+  constexpr int KK = D / 32;            // 32-channel slices of the score contraction
+  constexpr int NB = D / 16;            // 16-channel blocks of the output
+  constexpr int ROWB = D * 2;           // bytes of one V row
+  constexpr int PPR = D / 8;            // 16-byte pieces per V row
+  constexpr int RPI = 64 / PPR;         // V rows per 1 KiB DMA group
+  constexpr int VLD = 32 / RPI;         // DMA groups per step
+  constexpr int GPITCH = 1024 + (D == 128 ? 32 : 64);
+  constexpr int TILE = VLD * GPITCH;    // bytes of one step's V tile
+  constexpr int OPS = 2 * KK + VLD;     // vector-memory instructions issued per step
+  constexpr int STAGE_BYTES = NW * 2 * TILE;
   constexpr int MERGE_BYTES = NW * 16 * (D + 2) * 4;
   constexpr int SMEM = STAGE_BYTES > MERGE_BYTES ? STAGE_BYTES : MERGE_BYTES;
   __shared__ __align__(16) unsigned char smem[SMEM];
@@ -296,7 +308,7 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
   const int g = bg - b * a.hkv;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int c16 = lane & 15;
   const int j4 = lane >> 4;
   const int G = a.group;
@@ -342,60 +354,50 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 
-  unsigned char* vs = smem + wave * 32 * ROWB;
+  unsigned char* vtile[2] = {smem + (wave * 2) * TILE, smem + (wave * 2 + 1) * TILE};
   const int nsteps = (n_total + 31) >> 5;
 
-  struct Buf {
-    bf16x8 k[2][KK];
-    uint4 v[VLD];
+  // Row address of key i (keys past the end alias the current token's row).
+  auto krow = [&](int i) -> const uint16_t* {
+    return i < R.n_ring ? kring + (size_t)ring_slot(R, i) * D : knew;
   };
-
-  auto key_offset = [&](int i, bool& valid, bool& fresh) -> size_t {
-    valid = i < n_total;
-    fresh = i == R.n_ring;
-    return (i < R.n_ring) ? (size_t)ring_slot(R, i) * D : 0;
+  auto vrow = [&](int i) -> const uint16_t* {
+    return i < R.n_ring ? vring + (size_t)ring_slot(R, i) * D : vnew;
   };
+  // LDS piece swizzle of row-in-group rr (D = 64 only).
+  auto swz = [](int rr) -> int { return (D == 64 && rr >= 4) ? 2 : 0; };
 
-  auto load = [&](Buf& bf, int step) {
+  auto issue = [&](bf16x8 (&kb)[2][KK], unsigned char* tile, int step) {
     const int k0 = step * 32;
 #pragma unroll
     for (int tau = 0; tau < 2; ++tau) {
-      bool valid, fresh;
-      const size_t off = key_offset(k0 + 16 * tau + c16, valid, fresh);
-      const uint16_t* src = fresh ? knew : (kring + off);
+      const uint16_t* src = krow(k0 + 16 * tau + c16);
 #pragma unroll
-      for (int kk = 0; kk < KK; ++kk) {
-        if (valid) {
-          bf.k[tau][kk] = *(const bf16x8*)(src + 32 * kk + 8 * j4);
-        } else {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) bf.k[tau][kk][e] = (__bf16)0.0f;
-        }
-      }
+      for (int kk = 0; kk < KK; ++kk) kb[tau][kk] = *(const bf16x8*)(src + 32 * kk + 8 * j4);
     }
+    const int rr = lane / PPR;
+    const int piece = (lane % PPR) ^ swz(rr);
 #pragma unroll
     for (int x = 0; x < VLD; ++x) {
-      bool valid, fresh;
-      const size_t off = key_offset(k0 + x * RPI + lane / PPR, valid, fresh);
-      const uint16_t* src = fresh ? vnew : (vring + off);
-      bf.v[x] = valid ? *(const uint4*)(src + (lane % PPR) * 8) : make_uint4(0u, 0u, 0u, 0u);
+      const uint16_t* src = vrow(k0 + x * RPI + rr) + piece * 8;
+      __builtin_amdgcn_global_load_lds((const void*)src,
+                                       (__attribute__((address_space(3))) void*)(tile + x * GPITCH),
+                                       16, 0, 0);
     }
   };
 
-  auto compute = [&](const Buf& bf, int step) {
+  auto compute = [&](const bf16x8 (&kb)[2][KK], const unsigned char* tile, int step) {
+    // This step's K registers and V tile have landed once at most the next step's OPS
+    // loads remain outstanding (vmcnt retires in issue order).
+    __builtin_amdgcn_s_waitcnt(0x0F70 | (OPS & 15) | ((OPS >> 4) << 14));
     const int k0 = step * 32;
     f32x4 s0 = {0.0f, 0.0f, 0.0f, 0.0f};
     f32x4 s1 = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
-      s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bf.k[0][kk], qB[kk], s0, 0, 0, 0);
-      s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bf.k[1][kk], qB[kk], s1, 0, 0, 0);
+      s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb[0][kk], qB[kk], s0, 0, 0, 0);
+      s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb[1][kk], qB[kk], s1, 0, 0, 0);
     }
-    // Stage V (wave-private LDS tile, rows = keys of the step).
-#pragma unroll
-    for (int x = 0; x < VLD; ++x)
-      *(uint4*)(vs + (x * RPI + lane / PPR) * ROWB + (lane % PPR) * 16) = bf.v[x];
-
     float z[8];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
@@ -425,39 +427,48 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
     m = mn;
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) acc[nb] *= alpha;
-
-    __builtin_amdgcn_wave_barrier();
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
+      const int col = 16 * nb + c16;
       bf16x8 va;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const int row = e < 4 ? 4 * j4 + e : 16 + 4 * j4 + (e - 4);
-        va[e] = *(const __bf16*)(vs + row * ROWB + (16 * nb + c16) * 2);
+        const int rr = row % RPI;
+        const int off = (row / RPI) * GPITCH + rr * ROWB + (((col >> 3) ^ swz(rr)) << 4) +
+                        ((col & 7) << 1);
+        va[e] = *(const __bf16*)(tile + off);
       }
       acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pB, acc[nb], 0, 0, 0);
     }
-    __builtin_amdgcn_wave_barrier();
   };
 
-  Buf b0, b1;
+  // Software pipeline over this wave's steps.  The load for the step after the last one
+  // is still issued (every key past the end reads the current token's cached row), which
+  // keeps the issue count per iteration fixed for the vmcnt wait above.
+  bf16x8 k0r[2][KK], k1r[2][KK];
   int step = wave;
-  if (step < nsteps) load(b0, step);
+  issue(k0r, vtile[0], step);
   while (step < nsteps) {
-    if (step + NW < nsteps) load(b1, step + NW);
-    compute(b0, step);
+    issue(k1r, vtile[1], step + NW);
+    __builtin_amdgcn_sched_barrier(0);
+    compute(k0r, vtile[0], step);
+    __builtin_amdgcn_sched_barrier(0);
     step += NW;
     if (step >= nsteps) break;
-    if (step + NW < nsteps) load(b0, step + NW);
-    compute(b1, step);
+    issue(k0r, vtile[0], step + NW);
+    __builtin_amdgcn_sched_barrier(0);
+    compute(k1r, vtile[1], step);
+    __builtin_amdgcn_sched_barrier(0);
     step += NW;
   }
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // drain the trailing prefetch before LDS is reused
 
   // l per head: sum the four quarters' partial sums.
   lsum += __shfl_xor(lsum, 16);
   lsum += __shfl_xor(lsum, 32);
 
-  __syncthreads();  // every wave is done with its V tile: reuse LDS for the merge
+  __syncthreads();  // every wave is done with its V tiles: reuse LDS for the merge
   float* sm_acc = (float*)smem;              // [NW][16 heads][D]
   float* sm_m = sm_acc + NW * 16 * D;         // [NW][16]
   float* sm_l = sm_m + NW * 16;               // [NW][16]
