@@ -15,7 +15,7 @@
  *     support needs and retained entries never move (Sec. 3 "Flash-PBB"; Appendix F.1,
  *     Proposition "Relocation-free PBB cache").
  *   - The SWA baseline attends over {max(0, t-W+1) .. t} (Prop. 2, Sec. 2.2) stored in a
- *     ring of S >= W slots (Appendix F.1: a sliding window also admits a ring).
+ *     ring of S >= W slots (Appendix F.1 notes that a window can be kept in a ring as well).
  *
  * Layouts (row-major, contiguous, element type given by pbb_desc_t.dtype):
  *   q, out          [batch][n_q_heads][head_dim]
