@@ -27,6 +27,10 @@ namespace {
 
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 typedef __attribute__((ext_vector_type(4))) float f32x4;
+typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
+
+// Cache-policy operand of global_load_lds selecting the non-temporal ("nt") hint.
+constexpr int kCachePolicyNT = 2;
 
 constexpr float kNegInf = -__builtin_huge_valf();
 
@@ -373,7 +377,11 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
     for (int tau = 0; tau < 2; ++tau) {
       const uint16_t* src = krow(k0 + 16 * tau + c16);
 #pragma unroll
-      for (int kk = 0; kk < KK; ++kk) kb[tau][kk] = *(const bf16x8*)(src + 32 * kk + 8 * j4);
+      for (int kk = 0; kk < KK; ++kk) {
+        // Ring rows are read once per step: non-temporal loads skip cache allocation.
+        const u32x4 w = __builtin_nontemporal_load((const u32x4*)(src + 32 * kk + 8 * j4));
+        kb[tau][kk] = __builtin_bit_cast(bf16x8, w);
+      }
     }
     const int rr = lane / PPR;
     const int piece = (lane % PPR) ^ swz(rr);
@@ -382,7 +390,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
       const uint16_t* src = vrow(k0 + x * RPI + rr) + piece * 8;
       __builtin_amdgcn_global_load_lds((const void*)src,
                                        (__attribute__((address_space(3))) void*)(tile + x * GPITCH),
-                                       16, 0, 0);
+                                       16, 0, kCachePolicyNT);
     }
   };
 
