@@ -272,37 +272,44 @@ __global__ __launch_bounds__(256) void decode_f32_kernel(DecodeArgs a) {
 //
 // One workgroup of NW waves per (sequence, KV head); wave w handles 32-key steps
 // w, w + NW, ... of the unit's key list (ring keys, then the current token).  Per step:
-//   scores  S^T[16 keys][16 heads] = K Q^T with v_mfma_f32_16x16x32_bf16, two tiles.  The
-//           A operand (lane l: key l%16, 8 channels at 32kk + 8(l/16)) is loaded straight
-//           from the ring; the B operand is the group's queries, padded to 16 heads with 0.
+//   scores  S^T[16 keys][16 heads] = K Q^T with v_mfma_f32_16x16x32_bf16, two tiles; the A
+//           operand (lane l: key l%16, channels 32kk + 8(l/16) .. +7) is one 16-byte LDS read,
+//           the B operand holds the group's queries, padded to 16 heads with zeros.
 //   softmax lane (head h = l%16, quarter j = l/16) holds the scores of keys 4j..4j+3 and
 //           16+4j..16+4j+3; the running maximum is shared across the four quarters.
 //   values  O^T[16 channels][16 heads] += V^T P^T.  P^T's B operand is exactly the score
-//           registers (rounded to bf16), so the key order of the contraction is fixed by
-//           the score layout.  V rows go from HBM straight into a double-buffered,
-//           wave-private LDS tile (global_load_lds_dwordx4: no registers) and are read back
-//           transposed, one bf16 per lane and row.
-// The next step's K registers and V tile are in flight while the current step computes.
-// Every step issues the same number of loads (keys past the end read the current token's
-// row and are masked out of the softmax), so one vmcnt wait orders the LDS reads after the
-// tile's DMA.  Padded heads (h >= G) compute on zero queries and are never stored.  Wave
-// results are merged through LDS with Eq.(lse) (Appendix A.4) and written as bf16 (RNE).
+//           registers (rounded to bf16), so the key order of the contraction is fixed by the
+//           score layout; V is read back from LDS transposed, one bf16 per lane and row.
+// K and V rows travel from HBM straight into wave-private LDS tiles (global_load_lds_dwordx4
+// with the non-temporal hint: the ring is read once per step), two steps deep: while step s
+// computes, the loads of step s + NW are in flight, and step s + 2NW is issued right after.
+// No loaded value lands in a register, so the only memory wait is the explicit
+// vmcnt(OPS) at the top of a step: loads retire in issue order and exactly OPS loads (the
+// next step's) are issued after the current step's.  Steps past the end are still issued,
+// with every key reading the current token's cached row, to keep that count fixed.  Padded
+// heads (h >= G) compute on zero queries and are never stored.  Wave results are merged
+// through LDS with Eq.(lse) (Appendix A.4) and written as bf16 (RNE).
 //
-// V tile layout: the 32 rows of a step form 32/RPI groups of RPI rows, one group per 1 KiB
-// DMA (lane l lands at byte 16 l).  Group pitch and, for D = 64, a 16-byte piece swizzle in
-// the upper row quad make the transposed reads of rows 4j+e (j = 0..3) hit 32 distinct banks.
+// Tile layouts.  One 16-byte DMA of the wave writes 1 KiB: lane l lands at byte 16 l, i.e.
+// RPI whole rows.  K rows are contiguous; the 16-byte piece p of row r sits at piece slot
+// p ^ kswz(r), which spreads the 16 rows read by one MFMA operand over all banks.  V groups of
+// RPI rows are padded (and, for D = 64, the upper row quad is piece-swizzled) so that the
+// transposed reads of rows 4j+e (j = 0..3) hit 32 distinct banks.
 template <int D, int NW>
-__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) void decode_bf16_kernel(DecodeArgs a) {
+__global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
   constexpr int KK = D / 32;            // 32-channel slices of the score contraction
   constexpr int NB = D / 16;            // 16-channel blocks of the output
-  constexpr int ROWB = D * 2;           // bytes of one V row
-  constexpr int PPR = D / 8;            // 16-byte pieces per V row
-  constexpr int RPI = 64 / PPR;         // V rows per 1 KiB DMA group
-  constexpr int VLD = 32 / RPI;         // DMA groups per step
-  constexpr int GPITCH = 1024 + (D == 128 ? 32 : 64);
-  constexpr int TILE = VLD * GPITCH;    // bytes of one step's V tile
-  constexpr int OPS = 2 * KK + VLD;     // vector-memory instructions issued per step
-  constexpr int STAGE_BYTES = NW * 2 * TILE;
+  constexpr int ROWB = D * 2;           // bytes of one K or V row
+  constexpr int PPR = D / 8;            // 16-byte pieces per row
+  constexpr int RPI = 64 / PPR;         // rows per 1 KiB DMA group
+  constexpr int NG = 32 / RPI;          // DMA groups per step and tensor
+  constexpr int VPITCH = 1024 + (D == 128 ? 32 : 64);
+  constexpr int KTILE = 32 * ROWB;
+  constexpr int VTILE = NG * VPITCH;
+  constexpr int BUF = KTILE + VTILE;    // one step: K tile then V tile
+  constexpr int OPS = 2 * NG;           // DMA instructions per step
+  constexpr int QTILE = 16 * ROWB;      // the group's queries, 16 rows (heads >= G unused)
+  constexpr int STAGE_BYTES = NW * (2 * BUF + QTILE);
   constexpr int MERGE_BYTES = NW * 16 * (D + 2) * 4;
   constexpr int SMEM = STAGE_BYTES > MERGE_BYTES ? STAGE_BYTES : MERGE_BYTES;
   __shared__ __align__(16) unsigned char smem[SMEM];
@@ -329,82 +336,75 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
   const uint16_t* knew = (const uint16_t*)a.k_new + (size_t)bg * D;
   const uint16_t* vnew = (const uint16_t*)a.v_new + (size_t)bg * D;
 
-  // Fused append of the current token (slot t mod slots is outside the support).
-  if (wave == 0 && lane < 2 * PPR) {
-    const int piece = lane % PPR;
-    if (lane < PPR)
-      *(uint4*)(kring + (size_t)R.append_slot * D + piece * 8) = *(const uint4*)(knew + piece * 8);
-    else
-      *(uint4*)(vring + (size_t)R.append_slot * D + piece * 8) = *(const uint4*)(vnew + piece * 8);
-  }
 
   bf16x8 qB[KK];
-  {
-    const uint16_t* qrow = (const uint16_t*)a.q + ((size_t)b * a.hq + (size_t)g * G + c16) * D;
-#pragma unroll
-    for (int kk = 0; kk < KK; ++kk) {
-      if (c16 < G) {
-        qB[kk] = *(const bf16x8*)(qrow + 32 * kk + 8 * j4);
-      } else {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) qB[kk][e] = (__bf16)0.0f;
-      }
-    }
-  }
-
   float m = kNegInf;
   float lsum = 0.0f;
   f32x4 acc[NB];
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 
-  unsigned char* vtile[2] = {smem + (wave * 2) * TILE, smem + (wave * 2 + 1) * TILE};
+  unsigned char* buf[2] = {smem + (wave * 2) * BUF, smem + (wave * 2 + 1) * BUF};
+  unsigned char* qtile = smem + NW * 2 * BUF + wave * QTILE;
   const int nsteps = (n_total + 31) >> 5;
 
-  // Row address of key i (keys past the end alias the current token's row).
-  auto krow = [&](int i) -> const uint16_t* {
-    return i < R.n_ring ? kring + (size_t)ring_slot(R, i) * D : knew;
-  };
-  auto vrow = [&](int i) -> const uint16_t* {
-    return i < R.n_ring ? vring + (size_t)ring_slot(R, i) * D : vnew;
-  };
-  // LDS piece swizzle of row-in-group rr (D = 64 only).
-  auto swz = [](int rr) -> int { return (D == 64 && rr >= 4) ? 2 : 0; };
-
-  auto issue = [&](bf16x8 (&kb)[2][KK], unsigned char* tile, int step) {
-    const int k0 = step * 32;
+  // The group's query rows go to the wave's LDS query tile by the same DMA as K and V, ahead
+  // of the first K/V loads, so the first step's vmcnt wait covers them too (rows of heads
+  // >= G repeat head G-1 and are zeroed when read).
+  {
+    const uint16_t* qbase = (const uint16_t*)a.q + ((size_t)b * a.hq + (size_t)g * G) * D;
 #pragma unroll
-    for (int tau = 0; tau < 2; ++tau) {
-      const uint16_t* src = krow(k0 + 16 * tau + c16);
-#pragma unroll
-      for (int kk = 0; kk < KK; ++kk) {
-        // Ring rows are read once per step: non-temporal loads skip cache allocation.
-        const u32x4 w = __builtin_nontemporal_load((const u32x4*)(src + 32 * kk + 8 * j4));
-        kb[tau][kk] = __builtin_bit_cast(bf16x8, w);
-      }
-    }
-    const int rr = lane / PPR;
-    const int piece = (lane % PPR) ^ swz(rr);
-#pragma unroll
-    for (int x = 0; x < VLD; ++x) {
-      const uint16_t* src = vrow(k0 + x * RPI + rr) + piece * 8;
+    for (int x = 0; x < 16 / RPI; ++x) {
+      const int h = x * RPI + lane / PPR;
+      const uint16_t* src = qbase + (size_t)(h < G ? h : G - 1) * D + (lane % PPR) * 8;
       __builtin_amdgcn_global_load_lds((const void*)src,
-                                       (__attribute__((address_space(3))) void*)(tile + x * GPITCH),
+                                       (__attribute__((address_space(3))) void*)(qtile + x * 1024),
+                                       16, 0, 0);
+    }
+  }
+
+  // Row offset (elements) of key i in its ring, or of the current token's row.
+  auto row_of = [&](int i, const uint16_t* ring, const uint16_t* fresh) -> const uint16_t* {
+    return i < R.n_ring ? ring + (size_t)ring_slot(R, i) * D : fresh;
+  };
+  auto kswz = [](int r) -> int { return D == 128 ? (r & 15) : ((r >> 1) & 7); };
+  auto vswz = [](int rr) -> int { return (D == 64 && rr >= 4) ? 2 : 0; };
+
+  auto issue = [&](unsigned char* tile, int step) {
+    const int k0 = step * 32;
+    const int rr = lane / PPR;
+    const int slot = lane % PPR;
+#pragma unroll
+    for (int x = 0; x < NG; ++x) {
+      const int row = x * RPI + rr;
+      const uint16_t* src = row_of(k0 + row, kring, knew) + (slot ^ kswz(row)) * 8;
+      __builtin_amdgcn_global_load_lds((const void*)src,
+                                       (__attribute__((address_space(3))) void*)(tile + x * 1024),
                                        16, 0, kCachePolicyNT);
     }
+#pragma unroll
+    for (int x = 0; x < NG; ++x) {
+      const int row = x * RPI + rr;
+      const uint16_t* src = row_of(k0 + row, vring, vnew) + (slot ^ vswz(rr)) * 8;
+      __builtin_amdgcn_global_load_lds(
+          (const void*)src, (__attribute__((address_space(3))) void*)(tile + KTILE + x * VPITCH),
+          16, 0, kCachePolicyNT);
+    }
   };
 
-  auto compute = [&](const bf16x8 (&kb)[2][KK], const unsigned char* tile, int step) {
-    // This step's K registers and V tile have landed once at most the next step's OPS
-    // loads remain outstanding (vmcnt retires in issue order).
+  auto compute = [&](const unsigned char* tile, int step) {
+    // This step's tiles have landed once at most the next step's OPS loads are outstanding.
     __builtin_amdgcn_s_waitcnt(0x0F70 | (OPS & 15) | ((OPS >> 4) << 14));
     const int k0 = step * 32;
     f32x4 s0 = {0.0f, 0.0f, 0.0f, 0.0f};
     f32x4 s1 = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
-      s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb[0][kk], qB[kk], s0, 0, 0, 0);
-      s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb[1][kk], qB[kk], s1, 0, 0, 0);
+      const int p = 4 * kk + j4;
+      const bf16x8 ka = *(const bf16x8*)(tile + c16 * ROWB + ((p ^ kswz(c16)) << 4));
+      const bf16x8 kb = *(const bf16x8*)(tile + (16 + c16) * ROWB + ((p ^ kswz(16 + c16)) << 4));
+      s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qB[kk], s0, 0, 0, 0);
+      s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb, qB[kk], s1, 0, 0, 0);
     }
     float z[8];
 #pragma unroll
@@ -435,6 +435,7 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
     m = mn;
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) acc[nb] *= alpha;
+    const unsigned char* vt = tile + KTILE;
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
       const int col = 16 * nb + c16;
@@ -443,40 +444,51 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
       for (int e = 0; e < 8; ++e) {
         const int row = e < 4 ? 4 * j4 + e : 16 + 4 * j4 + (e - 4);
         const int rr = row % RPI;
-        const int off = (row / RPI) * GPITCH + rr * ROWB + (((col >> 3) ^ swz(rr)) << 4) +
+        const int off = (row / RPI) * VPITCH + rr * ROWB + (((col >> 3) ^ vswz(rr)) << 4) +
                         ((col & 7) << 1);
-        va[e] = *(const __bf16*)(tile + off);
+        va[e] = *(const __bf16*)(vt + off);
       }
       acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pB, acc[nb], 0, 0, 0);
     }
   };
 
-  // Software pipeline over this wave's steps.  The load for the step after the last one
-  // is still issued (every key past the end reads the current token's cached row), which
-  // keeps the issue count per iteration fixed for the vmcnt wait above.
-  bf16x8 k0r[2][KK], k1r[2][KK];
+  // Two-deep software pipeline with a uniform trip count (pairs of steps), then the odd one.
+  const int my_steps = wave < nsteps ? (nsteps - wave + NW - 1) / NW : 0;
   int step = wave;
-  issue(k0r, vtile[0], step);
-  while (step < nsteps) {
-    issue(k1r, vtile[1], step + NW);
+  issue(buf[0], step);
+  issue(buf[1], step + NW);
+  // Queries: wait until at most the two prefetched steps are outstanding, then read the
+  // B operand (channels 32kk + 8j .. +7 of head c16; zero for padded heads).
+  __builtin_amdgcn_s_waitcnt(0x0F70 | ((2 * OPS) & 15) | (((2 * OPS) >> 4) << 14));
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) {
+    const u32x4 zero = {0u, 0u, 0u, 0u};
+    const u32x4 w = *(const u32x4*)(qtile + c16 * ROWB + (4 * kk + j4) * 16);
+    qB[kk] = __builtin_bit_cast(bf16x8, c16 < G ? w : zero);
+  }
+  for (int pair = 0; pair < my_steps / 2; ++pair) {
     __builtin_amdgcn_sched_barrier(0);
-    compute(k0r, vtile[0], step);
+    compute(buf[0], step);
     __builtin_amdgcn_sched_barrier(0);
+    issue(buf[0], step + 2 * NW);
     step += NW;
-    if (step >= nsteps) break;
-    issue(k0r, vtile[0], step + NW);
     __builtin_amdgcn_sched_barrier(0);
-    compute(k1r, vtile[1], step);
+    compute(buf[1], step);
     __builtin_amdgcn_sched_barrier(0);
+    issue(buf[1], step + 2 * NW);
     step += NW;
   }
-  __builtin_amdgcn_s_waitcnt(0x0F70);  // drain the trailing prefetch before LDS is reused
+  if (my_steps & 1) {
+    __builtin_amdgcn_sched_barrier(0);
+    compute(buf[0], step);
+  }
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // drain the trailing prefetches before LDS is reused
 
   // l per head: sum the four quarters' partial sums.
   lsum += __shfl_xor(lsum, 16);
   lsum += __shfl_xor(lsum, 32);
 
-  __syncthreads();  // every wave is done with its V tiles: reuse LDS for the merge
+  __syncthreads();  // every wave is done with its tiles: reuse LDS for the merge
   float* sm_acc = (float*)smem;              // [NW][16 heads][D]
   float* sm_m = sm_acc + NW * 16 * D;         // [NW][16]
   float* sm_l = sm_m + NW * 16;               // [NW][16]
@@ -506,6 +518,17 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2))) vo
       O += wt * sm_acc[(w * 16 + h) * D + c];
     }
     out[idx] = float_to_bf16_rne(O / L);
+  }
+
+  // Fused append of the current token.  Slot t mod slots holds a position outside the support
+  // of t (and of every later step), so no read of this launch can observe the write; doing it
+  // last keeps its load off the streaming pipeline.
+  if (wave == 0 && lane < 2 * PPR) {
+    const int piece = lane % PPR;
+    if (lane < PPR)
+      *(uint4*)(kring + (size_t)R.append_slot * D + piece * 8) = *(const uint4*)(knew + piece * 8);
+    else
+      *(uint4*)(vring + (size_t)R.append_slot * D + piece * 8) = *(const uint4*)(vnew + piece * 8);
   }
 }
 
@@ -541,7 +564,7 @@ hipError_t launch_ring_fill(const int32_t* pos, const void* k_src, const void* v
 
 hipError_t launch_decode_bf16(const DecodeArgs& a, int32_t head_dim, hipStream_t stream) {
   const dim3 grid((unsigned)(a.batch * a.hkv));
-  constexpr int NW = 4;
+  constexpr int NW = 2;
   if (head_dim == 128)
     hipLaunchKernelGGL((decode_bf16_kernel<128, NW>), grid, dim3(NW * 64), 0, stream, a);
   else
