@@ -564,11 +564,21 @@ hipError_t launch_ring_fill(const int32_t* pos, const void* k_src, const void* v
 
 hipError_t launch_decode_bf16(const DecodeArgs& a, int32_t head_dim, hipStream_t stream) {
   const dim3 grid((unsigned)(a.batch * a.hkv));
-  constexpr int NW = 2;
-  if (head_dim == 128)
-    hipLaunchKernelGGL((decode_bf16_kernel<128, NW>), grid, dim3(NW * 64), 0, stream, a);
-  else
-    hipLaunchKernelGGL((decode_bf16_kernel<64, NW>), grid, dim3(NW * 64), 0, stream, a);
+  // Workgroup width: long supports (up to >= 2048 keys) stream best with 4 waves per unit and
+  // one workgroup per CU; shorter ones with 2 waves and two workgroups per CU (the LDS tiles
+  // of 8 waves do not fit one CU either way).
+  const int max_keys = a.mode == kSupportPBB ? a.block : a.window;
+  if (max_keys >= 2048) {
+    if (head_dim == 128)
+      hipLaunchKernelGGL((decode_bf16_kernel<128, 4>), grid, dim3(4 * 64), 0, stream, a);
+    else
+      hipLaunchKernelGGL((decode_bf16_kernel<64, 4>), grid, dim3(4 * 64), 0, stream, a);
+  } else {
+    if (head_dim == 128)
+      hipLaunchKernelGGL((decode_bf16_kernel<128, 2>), grid, dim3(2 * 64), 0, stream, a);
+    else
+      hipLaunchKernelGGL((decode_bf16_kernel<64, 2>), grid, dim3(2 * 64), 0, stream, a);
+  }
   return hipGetLastError();
 }
 

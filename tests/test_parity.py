@@ -131,6 +131,22 @@ def test_c5_swa_sampled(cuda):
     print(f"c5 {worst}")
 
 
+@pytest.mark.parametrize("mode,d,hq,hkv,block,window,slots", [
+    ("pbb", 64, 8, 2, 2048, 0, 2048),
+    ("pbb", 128, 16, 1, 4096, 0, 4096),
+    ("swa", 64, 4, 4, 0, 2048, 2048),
+    ("swa", 128, 6, 3, 0, 2500, 3000),
+])
+def test_long_support_shapes_sampled(cuda, mode, d, hq, hkv, block, window, slots):
+    """Supports of >= 2048 keys (the 4-wave workgroup variant) for both head dims, PBB and SWA,
+    pre-filled rings at edge and random positions."""
+    cfg = W.Config(f"long-{mode}-{d}-{hq}-{hkv}-{block}-{window}", mode, batch=40, hq=hq,
+                   hkv=hkv, d=d, block=block, slots=slots, window=window, dtype="bf16", seed=9,
+                   value_scale=1.0, pos_hi=300000, steps=2, prefill=True)
+    _, _, _, worst = _sampled(cfg, cuda, steps=2, n_rows=20)
+    print(f"{cfg.name} {worst}")
+
+
 def _support_variant(kind, t, B):
     h = B // 2
     p, r = B * (t // B), t % B
