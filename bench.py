@@ -138,6 +138,71 @@ class Workload:
         return elapsed, kern, total_bytes
 
 
+PAPER_ORIGINS = (8192, 16384, 32768, 65536, 131072, 262144, 524288, 1048576)
+
+
+def paper_latency(device, shapes=(10, 12, 14), origins=(8192,), steps=256, reps=9):
+    """The paper's latency-bound decode shape (batch 1, Hkv 2, head_dim 64, B 128; SWA w 128):
+    per (query heads, origin), 256 steps of decode + on-device position advance (one
+    ``*_decode_step_advance`` launch per step, alternating two position buffers) are captured as
+    one HIP graph and replayed ``reps`` times from the same restored state; the median replay
+    time / 256 is the per-step latency.  SWA runs in a 256-slot ring (the paper's SWA backend
+    allocated 256 positions) and in a 128-slot ring."""
+    import statistics
+
+    import torch
+    import paper_2606_02680_amd as P
+    import workloads as W
+    res = {}
+    for hq in shapes:
+        for origin in origins:
+            base = dict(batch=1, hq=hq, hkv=2, d=64, dtype="bf16", seed=11, value_scale=1.0,
+                        pos_hi=0, steps=steps, prefill=True)
+            cfgs = {"pbb_b128": W.Config("paper-pbb", "pbb", block=128, slots=128, window=0, **base),
+                    "swa_w128_s256": W.Config("paper-swa", "swa", block=128, slots=256, window=128,
+                                              **base),
+                    "swa_w128_s128": W.Config("paper-swa", "swa", block=128, slots=128, window=128,
+                                              **base)}
+            t0 = torch.tensor([origin], dtype=torch.int64)
+            cell = {}
+            inputs = None
+            for name, c in cfgs.items():
+                wl = Workload(c, t0, steps, device, inputs=inputs)
+                inputs = wl.inputs
+                snap = (wl.k_ring.clone(), wl.v_ring.clone(), wl.pos0.clone())
+                outs = torch.empty_like(inputs[0])
+                pos2 = (wl.pos, torch.empty_like(wl.pos))
+                adv = P.swa_decode_step_advance if c.mode == "swa" else P.pbb_decode_step_advance
+
+                def restore():
+                    wl.k_ring.copy_(snap[0]); wl.v_ring.copy_(snap[1]); pos2[0].copy_(snap[2])
+
+                restore()
+                g = torch.cuda.CUDAGraph()
+                torch.cuda.synchronize()
+                with torch.cuda.graph(g):
+                    # one kernel per step: decode + position advance into the other buffer
+                    for i in range(steps):
+                        adv(wl.desc, pos2[i % 2], pos2[(i + 1) % 2], inputs[0][i], inputs[1][i],
+                            inputs[2][i], wl.k_ring, wl.v_ring, outs[i])
+                times = []
+                for _ in range(reps + 1):
+                    restore()
+                    torch.cuda.synchronize()
+                    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                    e0.record()
+                    g.replay()
+                    e1.record()
+                    torch.cuda.synchronize()
+                    times.append(e0.elapsed_time(e1) * 1e3 / steps)
+                cell[f"{name}_us"] = statistics.median(times[1:])
+                del g, wl
+            cell["pbb_over_swa_s256"] = cell["swa_w128_s256_us"] / cell["pbb_b128_us"]
+            cell["pbb_over_swa_s128"] = cell["swa_w128_s128_us"] / cell["pbb_b128_us"]
+            res[f"hq{hq}_origin{origin}"] = cell
+    return res
+
+
 def cpu_baseline(cfg, t0, device, budget_s=12.0):
     """Time the fp64 CPU oracle on the first decode step of the workload's first sequences,
     repeating the sample until ``budget_s`` seconds have elapsed."""
@@ -187,6 +252,8 @@ def main(argv=None):
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extras", action="store_true",
                     help="skip the SWA-ring and ragged-batch comparison runs")
+    ap.add_argument("--paper-latency", action="store_true",
+                    help="only run the paper-shape latency sweep (3 shapes x 8 origins)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only time a plain 1 GiB device copy (HBM counter calibration)")
     args = ap.parse_args(argv)
@@ -217,6 +284,11 @@ def main(argv=None):
         el = (time.perf_counter() - w0) / 5
         print(json.dumps({"copy_probe_bytes_read": 2 * n, "copy_probe_bytes_written": 2 * n,
                           "copy_probe_gbps_read_plus_write": 4 * n / el / 1e9}), flush=True)
+        return 0
+
+    if args.paper_latency:
+        print(json.dumps({"paper_shape_latency_us_per_step":
+                          paper_latency(device, origins=PAPER_ORIGINS)}), flush=True)
         return 0
 
     cfg = W.get_config(args.config)
@@ -286,6 +358,9 @@ def main(argv=None):
                                    "hbm_gbps_kernel": tb / ext_steps / ks / 1e9,
                                    "frac_of_peak": tb / ext_steps / ks / 1e9 / HBM_PEAK_GBPS}
         del w4
+        torch.cuda.empty_cache()
+        extra["paper_shape_latency_us_per_step"] = paper_latency(
+            device, shapes=(10, 12, 14), origins=(8192, 1048576))
         result["extra"] = extra
         result["paper_context"] = ("Flash-PBB 1.82x Flash-SWA decode-core throughput on an RTX "
                                    "4090 (48 GB), BF16, batch 1, Hkv 2, d 64, b 128 vs w 128")

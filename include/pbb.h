@@ -141,6 +141,24 @@ pbb_status_t swa_decode_step(const pbb_desc_t *desc, const int32_t *pos, const v
                              const void *k_new, const void *v_new, void *k_ring, void *v_ring,
                              void *out, void *workspace, size_t workspace_bytes, void *stream);
 
+/*
+ * pbb_decode_step / swa_decode_step that also advance the positions on the device: the same
+ * launch writes pos_next[b] = pos[b] + 1 (pos[b] itself when pos[b] < 0).  pos is not written,
+ * and pos_next must not overlap pos (PBB_ERR_SHAPE), because other workgroups of the launch may
+ * still be reading pos; a caller alternates two position buffers between steps.  This keeps a
+ * step to a single kernel in captured graph sequences (the paper's decode runner advances
+ * positions on the device, Appendix F.7).  pos_next: int32 [batch], 4-byte aligned.
+ */
+pbb_status_t pbb_decode_step_advance(const pbb_desc_t *desc, const int32_t *pos, int32_t *pos_next,
+                                     const void *q, const void *k_new, const void *v_new,
+                                     void *k_ring, void *v_ring, void *out, void *workspace,
+                                     size_t workspace_bytes, void *stream);
+
+pbb_status_t swa_decode_step_advance(const pbb_desc_t *desc, const int32_t *pos, int32_t *pos_next,
+                                     const void *q, const void *k_new, const void *v_new,
+                                     void *k_ring, void *v_ring, void *out, void *workspace,
+                                     size_t workspace_bytes, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -47,20 +47,28 @@ size_t ring_tensor_bytes(const pbb_desc_t* d) {
          elem_bytes(d->dtype);
 }
 
-pbb_status_t decode_common(const pbb_desc_t* desc, bool swa, const int32_t* pos, const void* q,
-                           const void* k_new, const void* v_new, void* k_ring, void* v_ring,
-                           void* out, void* workspace, size_t workspace_bytes, void* stream) {
+pbb_status_t decode_common(const pbb_desc_t* desc, bool swa, const int32_t* pos, int32_t* pos_next,
+                           bool want_next, const void* q, const void* k_new, const void* v_new,
+                           void* k_ring, void* v_ring, void* out, void* workspace,
+                           size_t workspace_bytes, void* stream) {
   (void)workspace;
   (void)workspace_bytes;  // the selected kernels need no workspace
   const pbb_status_t st = check_desc(desc, swa);
   if (st != PBB_OK) return st;
   if (!pos || !q || !k_new || !v_new || !k_ring || !v_ring || !out) return PBB_ERR_NULL;
+  if (want_next && !pos_next) return PBB_ERR_NULL;
+  if (want_next && !aligned(pos_next, 4)) return PBB_ERR_ALIGN;
+  // pos_next must not overlap pos: other workgroups of the launch may still be reading pos.
+  if (want_next && (const void*)pos_next < (const void*)(pos + desc->batch) &&
+      (const void*)pos < (const void*)(pos_next + desc->batch))
+    return PBB_ERR_SHAPE;
   if (!aligned(pos, 4) || !aligned(q, 16) || !aligned(k_new, 16) || !aligned(v_new, 16) ||
       !aligned(k_ring, 16) || !aligned(v_ring, 16) || !aligned(out, 16))
     return PBB_ERR_ALIGN;
 
   pbb::DecodeArgs a;
   a.pos = pos;
+  a.pos_next = want_next ? pos_next : nullptr;
   a.q = q;
   a.k_new = k_new;
   a.v_new = v_new;
@@ -157,15 +165,31 @@ pbb_status_t swa_workspace_bytes(const pbb_desc_t* desc, size_t* bytes) {
 pbb_status_t pbb_decode_step(const pbb_desc_t* desc, const int32_t* pos, const void* q,
                              const void* k_new, const void* v_new, void* k_ring, void* v_ring,
                              void* out, void* workspace, size_t workspace_bytes, void* stream) {
-  return decode_common(desc, false, pos, q, k_new, v_new, k_ring, v_ring, out, workspace,
-                       workspace_bytes, stream);
+  return decode_common(desc, false, pos, nullptr, false, q, k_new, v_new, k_ring, v_ring, out,
+                       workspace, workspace_bytes, stream);
 }
 
 pbb_status_t swa_decode_step(const pbb_desc_t* desc, const int32_t* pos, const void* q,
                              const void* k_new, const void* v_new, void* k_ring, void* v_ring,
                              void* out, void* workspace, size_t workspace_bytes, void* stream) {
-  return decode_common(desc, true, pos, q, k_new, v_new, k_ring, v_ring, out, workspace,
-                       workspace_bytes, stream);
+  return decode_common(desc, true, pos, nullptr, false, q, k_new, v_new, k_ring, v_ring, out,
+                       workspace, workspace_bytes, stream);
+}
+
+pbb_status_t pbb_decode_step_advance(const pbb_desc_t* desc, const int32_t* pos, int32_t* pos_next,
+                                     const void* q, const void* k_new, const void* v_new,
+                                     void* k_ring, void* v_ring, void* out, void* workspace,
+                                     size_t workspace_bytes, void* stream) {
+  return decode_common(desc, false, pos, pos_next, true, q, k_new, v_new, k_ring, v_ring, out,
+                       workspace, workspace_bytes, stream);
+}
+
+pbb_status_t swa_decode_step_advance(const pbb_desc_t* desc, const int32_t* pos, int32_t* pos_next,
+                                     const void* q, const void* k_new, const void* v_new,
+                                     void* k_ring, void* v_ring, void* out, void* workspace,
+                                     size_t workspace_bytes, void* stream) {
+  return decode_common(desc, true, pos, pos_next, true, q, k_new, v_new, k_ring, v_ring, out,
+                       workspace, workspace_bytes, stream);
 }
 
 }  // extern "C"

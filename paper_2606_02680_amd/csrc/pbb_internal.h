@@ -13,6 +13,7 @@ enum SupportMode : int32_t { kSupportPBB = 0, kSupportSWA = 1 };
 // Everything a decode kernel needs, validated on the host before launch.
 struct DecodeArgs {
   const int32_t* pos;
+  int32_t* pos_next;   // optional: receives pos + 1 (pos itself for pos < 0); never aliases pos
   const void* q;
   const void* k_new;
   const void* v_new;

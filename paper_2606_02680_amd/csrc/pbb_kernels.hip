@@ -143,9 +143,11 @@ __global__ __launch_bounds__(256) void decode_f32_kernel(DecodeArgs a) {
   const int t = a.pos[b];
   if (t < 0) {
     for (int e = tid; e < G * D; e += 256) out[e] = 0.0f;
+    if (a.pos_next != nullptr && g == 0 && tid == 0) a.pos_next[b] = t;
     return;
   }
   const Ranges R = ranges_for(a, t);
+  if (a.pos_next != nullptr && g == 0 && tid == 0) a.pos_next[b] = t + 1;
   float* kring = (float*)a.k_ring + (size_t)bg * a.slots * D;
   float* vring = (float*)a.v_ring + (size_t)bg * a.slots * D;
   const float* knew = (const float*)a.k_new + (size_t)bg * D;
@@ -295,8 +297,11 @@ __global__ __launch_bounds__(256) void decode_f32_kernel(DecodeArgs a) {
 // p ^ kswz(r), which spreads the 16 rows read by one MFMA operand over all banks.  V groups of
 // RPI rows are padded (and, for D = 64, the upper row quad is piece-swizzled) so that the
 // transposed reads of rows 4j+e (j = 0..3) hit 32 distinct banks.
-template <int D, int NW>
+template <int D, int NW, bool NT>
 __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
+  // NT: stream the ring with the non-temporal hint (rings far larger than the caches); without
+  // it, small rings that are re-read every step can stay cache-resident.
+  constexpr int kPolicy = NT ? kCachePolicyNT : 0;
   constexpr int KK = D / 32;            // 32-channel slices of the score contraction
   constexpr int NB = D / 16;            // 16-channel blocks of the output
   constexpr int ROWB = D * 2;           // bytes of one K or V row
@@ -327,6 +332,7 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
   const int t = a.pos[b];
   if (t < 0) {
     for (int e = tid; e < G * D; e += NW * 64) out[e] = 0;
+    if (a.pos_next != nullptr && g == 0 && tid == 0) a.pos_next[b] = t;
     return;
   }
   const Ranges R = ranges_for(a, t);
@@ -335,7 +341,14 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
   uint16_t* vring = (uint16_t*)a.v_ring + (size_t)bg * a.slots * D;
   const uint16_t* knew = (const uint16_t*)a.k_new + (size_t)bg * D;
   const uint16_t* vnew = (const uint16_t*)a.v_new + (size_t)bg * D;
+  if (a.pos_next != nullptr && g == 0 && tid == 0) a.pos_next[b] = t + 1;
 
+  // The current token's row for the append: loaded now, stored at the end, so that only the
+  // store sits on the tail of a latency-bound launch.
+  const bool appender = wave == 0 && lane < 2 * PPR;
+  u32x4 append_row = {0u, 0u, 0u, 0u};
+  if (appender)
+    append_row = *(const u32x4*)((lane < PPR ? knew : vnew) + (lane % PPR) * 8);
 
   bf16x8 qB[KK];
   float m = kNegInf;
@@ -380,7 +393,7 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
       const uint16_t* src = row_of(k0 + row, kring, knew) + (slot ^ kswz(row)) * 8;
       __builtin_amdgcn_global_load_lds((const void*)src,
                                        (__attribute__((address_space(3))) void*)(tile + x * 1024),
-                                       16, 0, kCachePolicyNT);
+                                       16, 0, kPolicy);
     }
 #pragma unroll
     for (int x = 0; x < NG; ++x) {
@@ -388,7 +401,7 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
       const uint16_t* src = row_of(k0 + row, vring, vnew) + (slot ^ vswz(rr)) * 8;
       __builtin_amdgcn_global_load_lds(
           (const void*)src, (__attribute__((address_space(3))) void*)(tile + KTILE + x * VPITCH),
-          16, 0, kCachePolicyNT);
+          16, 0, kPolicy);
     }
   };
 
@@ -521,15 +534,10 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
   }
 
   // Fused append of the current token.  Slot t mod slots holds a position outside the support
-  // of t (and of every later step), so no read of this launch can observe the write; doing it
-  // last keeps its load off the streaming pipeline.
-  if (wave == 0 && lane < 2 * PPR) {
-    const int piece = lane % PPR;
-    if (lane < PPR)
-      *(uint4*)(kring + (size_t)R.append_slot * D + piece * 8) = *(const uint4*)(knew + piece * 8);
-    else
-      *(uint4*)(vring + (size_t)R.append_slot * D + piece * 8) = *(const uint4*)(vnew + piece * 8);
-  }
+  // of t (and of every later step), so no read of this launch can observe the write.
+  if (appender)
+    *(u32x4*)((lane < PPR ? kring : vring) + (size_t)R.append_slot * D + (lane % PPR) * 8) =
+        append_row;
 }
 
 }  // namespace
@@ -562,22 +570,31 @@ hipError_t launch_ring_fill(const int32_t* pos, const void* k_src, const void* v
   return hipGetLastError();
 }
 
-hipError_t launch_decode_bf16(const DecodeArgs& a, int32_t head_dim, hipStream_t stream) {
+template <int D, int NW>
+void launch_bf16_policy(const DecodeArgs& a, bool nt, hipStream_t stream) {
   const dim3 grid((unsigned)(a.batch * a.hkv));
+  if (nt)
+    hipLaunchKernelGGL((decode_bf16_kernel<D, NW, true>), grid, dim3(NW * 64), 0, stream, a);
+  else
+    hipLaunchKernelGGL((decode_bf16_kernel<D, NW, false>), grid, dim3(NW * 64), 0, stream, a);
+}
+
+hipError_t launch_decode_bf16(const DecodeArgs& a, int32_t head_dim, hipStream_t stream) {
   // Workgroup width: long supports (up to >= 2048 keys) stream best with 4 waves per unit and
-  // one workgroup per CU; shorter ones with 2 waves and two workgroups per CU (the LDS tiles
-  // of 8 waves do not fit one CU either way).
+  // one workgroup per CU; so do launches with fewer units than CUs, where the latency of a
+  // unit is what counts.  Otherwise 2 waves and two workgroups per CU.
   const int max_keys = a.mode == kSupportPBB ? a.block : a.window;
-  if (max_keys >= 2048) {
-    if (head_dim == 128)
-      hipLaunchKernelGGL((decode_bf16_kernel<128, 4>), grid, dim3(4 * 64), 0, stream, a);
-    else
-      hipLaunchKernelGGL((decode_bf16_kernel<64, 4>), grid, dim3(4 * 64), 0, stream, a);
+  const int units = a.batch * a.hkv;
+  const bool wide = max_keys >= 2048 || units < 256;
+  // Non-temporal loads once both rings exceed the 256 MiB last-level cache of the chip.
+  const double ring_bytes = 4.0 * (double)units * (double)a.slots * (double)head_dim;
+  const bool nt = ring_bytes > 256.0 * 1024.0 * 1024.0;
+  if (head_dim == 128) {
+    if (wide) launch_bf16_policy<128, 4>(a, nt, stream);
+    else launch_bf16_policy<128, 2>(a, nt, stream);
   } else {
-    if (head_dim == 128)
-      hipLaunchKernelGGL((decode_bf16_kernel<128, 2>), grid, dim3(2 * 64), 0, stream, a);
-    else
-      hipLaunchKernelGGL((decode_bf16_kernel<64, 2>), grid, dim3(2 * 64), 0, stream, a);
+    if (wide) launch_bf16_policy<64, 4>(a, nt, stream);
+    else launch_bf16_policy<64, 2>(a, nt, stream);
   }
   return hipGetLastError();
 }

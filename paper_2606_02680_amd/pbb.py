@@ -23,7 +23,8 @@ DTYPE_BF16 = 1
 _TORCH_DTYPE = {DTYPE_F32: torch.float32, DTYPE_BF16: torch.bfloat16}
 
 EXPORTS = ("pbb_status_string", "pbb_ring_bytes", "pbb_ring_init", "pbb_ring_fill",
-           "pbb_workspace_bytes", "pbb_decode_step", "swa_workspace_bytes", "swa_decode_step")
+           "pbb_workspace_bytes", "pbb_decode_step", "swa_workspace_bytes", "swa_decode_step",
+           "pbb_decode_step_advance", "swa_decode_step_advance")
 
 
 class PbbError(RuntimeError):
@@ -71,6 +72,8 @@ def load_library(path: str = _LIB_PATH):
     lib.swa_workspace_bytes.argtypes = [dp, ctypes.POINTER(sz)]
     for fn in ("pbb_decode_step", "swa_decode_step"):
         getattr(lib, fn).argtypes = [dp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    for fn in ("pbb_decode_step_advance", "swa_decode_step_advance"):
+        getattr(lib, fn).argtypes = [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     for fn in EXPORTS[1:]:
         getattr(lib, fn).restype = ctypes.c_int
     _lib = lib
@@ -174,8 +177,10 @@ def ring_fill(desc: PbbDesc, pos: torch.Tensor, k_src: torch.Tensor, v_src: torc
 
 
 def _decode(fn: str, desc: PbbDesc, pos, q, k_new, v_new, k_ring, v_ring, out, workspace,
-            stream):
+            stream, pos_next=None):
     _expect("pos", pos, (desc.batch,), torch.int32)
+    if pos_next is not None:
+        _expect("pos_next", pos_next, (desc.batch,), torch.int32)
     _expect("q", q, (desc.batch, desc.n_q_heads, desc.head_dim), desc.torch_dtype)
     _expect("out", out, (desc.batch, desc.n_q_heads, desc.head_dim), desc.torch_dtype)
     for n, t in (("k_new", k_new), ("v_new", v_new)):
@@ -183,8 +188,9 @@ def _decode(fn: str, desc: PbbDesc, pos, q, k_new, v_new, k_ring, v_ring, out, w
     for n, t in (("k_ring", k_ring), ("v_ring", v_ring)):
         _expect(n, t, ring_shape(desc), desc.torch_dtype)
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    extra = () if pos_next is None else (_ptr(pos_next),)
     _check(fn, getattr(load_library(), fn)(
-        ctypes.byref(desc), _ptr(pos), _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(k_ring),
+        ctypes.byref(desc), _ptr(pos), *extra, _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(k_ring),
         _ptr(v_ring), _ptr(out), _ptr(workspace), ctypes.c_size_t(ws_bytes), _stream(stream)))
     return out
 
@@ -201,6 +207,20 @@ def swa_decode_step(desc: PbbDesc, pos, q, k_new, v_new, k_ring, v_ring, out, wo
     """Fused ring append + sliding-window attention (baseline, same kernels)."""
     return _decode("swa_decode_step", desc, pos, q, k_new, v_new, k_ring, v_ring, out, workspace,
                    stream)
+
+
+def pbb_decode_step_advance(desc: PbbDesc, pos, pos_next, q, k_new, v_new, k_ring, v_ring, out,
+                            workspace=None, stream=None):
+    """:func:`pbb_decode_step` that also writes ``pos_next = pos + 1`` (``pos`` unchanged)."""
+    return _decode("pbb_decode_step_advance", desc, pos, q, k_new, v_new, k_ring, v_ring, out,
+                   workspace, stream, pos_next=pos_next)
+
+
+def swa_decode_step_advance(desc: PbbDesc, pos, pos_next, q, k_new, v_new, k_ring, v_ring, out,
+                            workspace=None, stream=None):
+    """:func:`swa_decode_step` that also writes ``pos_next = pos + 1`` (``pos`` unchanged)."""
+    return _decode("swa_decode_step_advance", desc, pos, q, k_new, v_new, k_ring, v_ring, out,
+                   workspace, stream, pos_next=pos_next)
 
 
 def default_scale(head_dim: int) -> float:

@@ -93,6 +93,26 @@ def test_alignment_errors(name):
     assert _decode(_desc(window=64, slots=64), "swa_decode_step", **{name: A + 2}) == 4
 
 
+def _advance(desc, fn="pbb_decode_step_advance", **ptrs):
+    args = dict(pos=A, pos_next=A + 4096, q=A, k_new=A, v_new=A, k_ring=A, v_ring=A, out=A)
+    args.update(ptrs)
+    vp = ctypes.c_void_p
+    return getattr(B.load_library(), fn)(
+        ctypes.byref(desc), vp(args["pos"]), vp(args["pos_next"]), vp(args["q"]),
+        vp(args["k_new"]), vp(args["v_new"]), vp(args["k_ring"]), vp(args["v_ring"]),
+        vp(args["out"]), vp(0), ctypes.c_size_t(0), vp(0))
+
+
+@pytest.mark.parametrize("fn", ["pbb_decode_step_advance", "swa_decode_step_advance"])
+def test_advance_argument_errors(fn):
+    desc = _desc(window=32, slots=64) if fn.startswith("swa") else _desc()
+    assert _advance(desc, fn, pos_next=0) == 1
+    assert _advance(desc, fn, pos_next=A + 4098) == 4
+    assert _advance(desc, fn, pos_next=A) == 2          # aliases pos
+    assert _advance(desc, fn, pos_next=A + 4) == 2      # overlaps pos[1] (batch 2)
+    assert _advance(desc, fn, q=A + 2) == 4
+
+
 def test_pos_alignment():
     assert _decode(_desc(), pos=A + 2) == 4
 
