@@ -92,6 +92,7 @@ class Workload:
             self.desc = P.make_desc(cfg.batch, cfg.hq, cfg.hkv, cfg.d, block=cfg.block, dtype=dt)
             self.fn = P.pbb_decode_step
         self.k_ring, self.v_ring = P.alloc_rings(self.desc, device)
+        self.ws = P.alloc_workspace(self.desc, device)
         P.ring_init(self.desc, self.k_ring, self.v_ring)
         self.pos0 = t0.to(torch.int32).to(device)
         self.pos = self.pos0.clone()
@@ -110,7 +111,7 @@ class Workload:
 
     def step(self, i):
         q, k, v = self.inputs[0][i], self.inputs[1][i], self.inputs[2][i]
-        self.fn(self.desc, self.pos, q, k, v, self.k_ring, self.v_ring, self.out)
+        self.fn(self.desc, self.pos, q, k, v, self.k_ring, self.v_ring, self.out, self.ws)
 
     def timed(self, warmup, steps):
         """Returns (elapsed seconds of the whole loop, mean kernel seconds, algorithmic bytes)."""
@@ -184,7 +185,7 @@ def paper_latency(device, shapes=(10, 12, 14), origins=(8192,), steps=256, reps=
                     # one kernel per step: decode + position advance into the other buffer
                     for i in range(steps):
                         adv(wl.desc, pos2[i % 2], pos2[(i + 1) % 2], inputs[0][i], inputs[1][i],
-                            inputs[2][i], wl.k_ring, wl.v_ring, outs[i])
+                            inputs[2][i], wl.k_ring, wl.v_ring, outs[i], wl.ws)
                 times = []
                 for _ in range(reps + 1):
                     restore()

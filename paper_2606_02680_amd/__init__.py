@@ -4,6 +4,6 @@ The product is ``libpbb.so`` (C ABI in ``include/pbb.h``, HIP kernels for gfx950
 ``csrc/``); :mod:`paper_2606_02680_amd.pbb` is its thin ctypes binding.
 """
 from .pbb import (  # noqa: F401
-    PbbDesc, PbbError, alloc_rings, load_library, make_desc, pbb_decode_step,
+    PbbDesc, PbbError, alloc_rings, alloc_workspace, load_library, make_desc, pbb_decode_step,
     pbb_decode_step_advance, ring_bytes, ring_fill, ring_init, swa_decode_step,
     swa_decode_step_advance, swa_workspace_bytes, workspace_bytes)

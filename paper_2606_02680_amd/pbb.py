@@ -144,6 +144,14 @@ def swa_workspace_bytes(desc: PbbDesc) -> int:
     return out.value
 
 
+def alloc_workspace(desc: PbbDesc, device="cuda"):
+    """Zero-filled workspace for the decode calls of ``desc`` (PBB or SWA rules by
+    ``desc.window``), or None when they need none.  Launches leave it zeroed, so one allocation
+    serves every later call on one stream."""
+    n = swa_workspace_bytes(desc) if desc.window > 0 else workspace_bytes(desc)
+    return torch.zeros(n, dtype=torch.uint8, device=device) if n > 0 else None
+
+
 def ring_shape(desc: PbbDesc):
     return (desc.batch, desc.n_kv_heads, desc.slots, desc.head_dim)
 

@@ -81,6 +81,7 @@ class Run:
     def __post_init__(self):
         self.desc = desc_for(self.cfg, batch=self.t0.numel())
         self.k_ring, self.v_ring = P.alloc_rings(self.desc, self.device)
+        self.ws = P.alloc_workspace(self.desc, self.device)
         P.ring_init(self.desc, self.k_ring, self.v_ring)
         self.pos = self.t0.to(torch.int32).to(self.device)
         if self.cfg.prefill:
@@ -120,7 +121,7 @@ class Run:
         q, k, v = self.step_inputs(self.step_index) if inputs is None else inputs
         out = torch.empty_like(q)
         fn = P.swa_decode_step if self.cfg.mode == "swa" else P.pbb_decode_step
-        fn(self.desc, self.pos, q, k, v, self.k_ring, self.v_ring, out)
+        fn(self.desc, self.pos, q, k, v, self.k_ring, self.v_ring, out, self.ws)
         self.pos += 1
         self.step_index += 1
         return q, out
