@@ -15,6 +15,8 @@ Layers?"):
 * Sec. 3, Eq.(attention) -- one softmax over the support with scores ``q.k / sqrt(d_h)``.
 * Appendix F.1, Proposition "Relocation-free PBB cache" -- position ``s`` is stored at slot
   ``s mod b``; :func:`expected_ring` gives the ring image that sequential appends produce.
+* Appendix A.4, Eq.(lse) -- the log-partition ``log sum_s e^{z_s}`` that :func:`prefill` also
+  returns for every prompt position (the quantity a tiled prefill rescales with).
 
 The arithmetic lives in ``pbb_oracle.c`` (fp64, plain loops, threads over (sequence, query
 head)); this module is argument marshalling plus the ring-image rule.  Inputs are float32
@@ -73,6 +75,9 @@ def _load():
     lib.oracle_decode.argtypes = [i32, i64, i64, i64, i64, i64, i64, vp, vp, vp, vp, vp, i64,
                                   dbl, vp, i32]
     lib.oracle_decode.restype = i32
+    lib.oracle_prefill.argtypes = [i32, i64, i64, i64, i64, i64, i64, i64, vp, vp, vp, dbl, vp,
+                                   vp, i32]
+    lib.oracle_prefill.restype = i32
     _lib = lib
     return lib
 
@@ -176,6 +181,33 @@ def decode(mode: int, pos, q, k_hist, v_hist, hist_lo, *, block: int = 0, window
     if rc != 0:
         raise ValueError("oracle.decode: invalid arguments")
     return out
+
+
+def prefill(mode: int, q, k, v, *, block: int = 0, window: int = 0, scale: float | None = None,
+            n_threads: int = 0):
+    """Prefill of prompts at positions ``0 .. n-1`` in fp64: every position attends over its
+    own support (Eq.(pbb) with ``h = block/2`` for :data:`PBB`, Prop. 2 for :data:`SWA`).
+
+    ``q``: [batch][n][Hq][d]; ``k``/``v``: [batch][n][Hkv][d] (token-major).  Returns
+    ``(out, lse)``: float64 [batch][n][Hq][d] and the log-partition ``log sum_s e^{z_s}``
+    (Appendix A.4, Eq.(lse)) as float64 [batch][Hq][n].
+    """
+    q = np.ascontiguousarray(q, dtype=np.float32)
+    k = np.ascontiguousarray(k, dtype=np.float32)
+    v = np.ascontiguousarray(v, dtype=np.float32)
+    batch, n, hq, d = q.shape
+    assert k.shape == v.shape and k.shape[:2] == (batch, n) and k.shape[3] == d
+    hkv = k.shape[2]
+    if scale is None:
+        scale = 1.0 / np.sqrt(d)
+    out = np.zeros((batch, n, hq, d), dtype=np.float64)
+    lse = np.zeros((batch, hq, n), dtype=np.float64)
+    rc = _load().oracle_prefill(int(mode), batch, n, hq, hkv, d, int(block), int(window),
+                                _ptr(q), _ptr(k), _ptr(v), float(scale), _ptr(out), _ptr(lse),
+                                int(n_threads))
+    if rc != 0:
+        raise ValueError("oracle.prefill: invalid arguments")
+    return out, lse
 
 
 # ----------------------------------------------------------------------------------------

@@ -12,6 +12,8 @@
  *       A(t) = {p..t}  union  {p-h..p-1} if p > 0 and 0 <= r < h, else nothing
  *   - the sliding-window support {max(0,t-w+1)..t}                         Prop. 2 (Sec. 2.2)
  *   - single-softmax attention over a support, scores q.k/sqrt(d)          Sec. 3, Eq.(attention)
+ *   - prefill: every prompt position over its own support, with its log-partition
+ *     log sum_s e^{z_s}                                                    Appendix A.4, Eq.(lse)
  * Keys and values are read from HISTORY arrays indexed by absolute position, never from
  * a ring, and every sum is taken in fp64 in plain position order.
  */
@@ -240,4 +242,126 @@ int oracle_decode(int mode, int64_t batch, int64_t n_q_heads, int64_t n_kv_heads
     for (int i = 0; i < n_threads; ++i) pthread_join(th[i], NULL);
     pthread_mutex_destroy(&j.lock);
     return j.error ? 1 : 0;
+}
+
+/* ------------------------------------------------------------------------------------ */
+/* Prefill: every position of a prompt attends over its own support.                     */
+
+typedef struct {
+    int mode; /* 0 = PBB, 1 = SWA */
+    int64_t batch, n, n_q_heads, n_kv_heads, head_dim, block, window;
+    const float *q; /* [batch][n][Hq][d] */
+    const float *k; /* [batch][n][Hkv][d], position s of sequence b at row s */
+    const float *v;
+    double scale;
+    double *out; /* [batch][n][Hq][d] */
+    double *lse; /* [batch][Hq][n] */
+    int64_t next;
+    pthread_mutex_t lock;
+} prefill_job;
+
+static int prefill_member(const prefill_job *j, int64_t t, int64_t s) {
+    if (j->mode == 0) return oracle_pbb_member(t, s, j->block, j->block / 2);
+    return oracle_swa_member(t, s, j->window);
+}
+
+/* One (sequence, position, query head): scores over the support in position order, then
+ * o = sum_s e^{z_s - m} v_s / sum_s e^{z_s - m} and lse = m + log sum_s e^{z_s - m}. */
+static void prefill_one(prefill_job *j, int64_t item, double *z, double *qd) {
+    const int64_t d = j->head_dim, hq = j->n_q_heads, hkv = j->n_kv_heads, n = j->n;
+    const int64_t G = hq / hkv;
+    const int64_t i = item % hq;
+    const int64_t t = (item / hq) % n;
+    const int64_t b = item / (hq * n);
+    const int64_t g = i / G; /* query head i reads KV head floor(i/G) */
+    double *o = j->out + ((b * n + t) * hq + i) * d;
+    for (int64_t c = 0; c < d; ++c) {
+        o[c] = 0.0;
+        qd[c] = (double)j->q[((b * n + t) * hq + i) * d + c];
+    }
+    const int64_t span = (j->mode == 0) ? (j->block + j->block / 2) : j->window;
+    int64_t lo = t - span;
+    if (lo < 0) lo = 0;
+    double m = -INFINITY;
+    for (int64_t s = lo; s <= t; ++s) {
+        if (!prefill_member(j, t, s)) continue;
+        const float *ks = j->k + ((b * n + s) * hkv + g) * d;
+        double acc = 0.0;
+        for (int64_t c = 0; c < d; ++c) acc += qd[c] * (double)ks[c];
+        z[s - lo] = acc * j->scale;
+        if (z[s - lo] > m) m = z[s - lo];
+    }
+    double den = 0.0;
+    for (int64_t s = lo; s <= t; ++s) {
+        if (!prefill_member(j, t, s)) continue;
+        const float *vs = j->v + ((b * n + s) * hkv + g) * d;
+        double w = exp(z[s - lo] - m);
+        den += w;
+        for (int64_t c = 0; c < d; ++c) o[c] += w * (double)vs[c];
+    }
+    for (int64_t c = 0; c < d; ++c) o[c] /= den;
+    j->lse[(b * hq + i) * n + t] = m + log(den);
+}
+
+static void *prefill_worker(void *arg) {
+    prefill_job *j = (prefill_job *)arg;
+    int64_t span = (j->mode == 0) ? (j->block + j->block / 2) : j->window;
+    double *z = (double *)malloc(sizeof(double) * (size_t)(span + 1));
+    double *qd = (double *)malloc(sizeof(double) * (size_t)j->head_dim);
+    const int64_t total = j->batch * j->n * j->n_q_heads;
+    for (;;) {
+        pthread_mutex_lock(&j->lock);
+        int64_t first = j->next;
+        j->next += 64;
+        pthread_mutex_unlock(&j->lock);
+        if (first >= total) break;
+        int64_t last = first + 64 < total ? first + 64 : total;
+        for (int64_t item = first; item < last; ++item) prefill_one(j, item, z, qd);
+    }
+    free(z);
+    free(qd);
+    return NULL;
+}
+
+/*
+ * Prefill of a batch of prompts of n tokens at positions 0..n-1: for every sequence b,
+ * position t and query head i, attention of q[b][t][i] over the support of t (PBB with
+ * h = block/2 when mode == 0, Eq.(pbb); SWA with the given window when mode == 1, Prop. 2),
+ * Eq.(attention), plus the log-partition lse = log sum_{s in A(t)} e^{z_s} (Appendix A.4,
+ * Eq.(lse)).  Layouts: q, out [batch][n][Hq][d]; k, v [batch][n][Hkv][d]; lse [batch][Hq][n].
+ * Returns 0 on success, 2 on bad arguments.  n_threads <= 0 uses every online core.
+ */
+int oracle_prefill(int mode, int64_t batch, int64_t n, int64_t n_q_heads, int64_t n_kv_heads,
+                   int64_t head_dim, int64_t block, int64_t window, const float *q,
+                   const float *k, const float *v, double scale, double *out, double *lse,
+                   int n_threads) {
+    if (batch < 0 || n < 0 || n_q_heads <= 0 || n_kv_heads <= 0 || head_dim <= 0) return 2;
+    if (n_q_heads % n_kv_heads != 0) return 2;
+    if (mode == 0 && (block < 2 || block % 2 != 0)) return 2;
+    if (mode == 1 && window < 1) return 2;
+    prefill_job j;
+    memset(&j, 0, sizeof(j));
+    j.mode = mode;
+    j.batch = batch;
+    j.n = n;
+    j.n_q_heads = n_q_heads;
+    j.n_kv_heads = n_kv_heads;
+    j.head_dim = head_dim;
+    j.block = block;
+    j.window = window;
+    j.q = q;
+    j.k = k;
+    j.v = v;
+    j.scale = scale;
+    j.out = out;
+    j.lse = lse;
+    pthread_mutex_init(&j.lock, NULL);
+    if (n_threads <= 0) n_threads = (int)sysconf(_SC_NPROCESSORS_ONLN);
+    if (n_threads < 1) n_threads = 1;
+    if (n_threads > 256) n_threads = 256;
+    pthread_t th[256];
+    for (int i = 0; i < n_threads; ++i) pthread_create(&th[i], NULL, prefill_worker, &j);
+    for (int i = 0; i < n_threads; ++i) pthread_join(th[i], NULL);
+    pthread_mutex_destroy(&j.lock);
+    return 0;
 }
