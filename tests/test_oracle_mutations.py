@@ -22,9 +22,12 @@ MUTATIONS = {
     "bridge_start_off_by_one": ("s >= p - bridge && s <= p - 1", "s > p - bridge && s <= p - 1"),
     "block_start_dropped": ("if (s >= p) return 1;", "if (s > p) return 1;"),
     "bridge_wrong_half": ("s >= p - bridge && s <= p - 1", "s >= p - 2 * bridge && s <= p - bridge - 1"),
-    "scale_dropped": ("z[s - lo] = acc * j->scale;", "z[s - lo] = acc;"),
-    "exp_sign_flipped": ("double w = exp(z[s - lo] - m);", "double w = exp(m - z[s - lo]);"),
-    "gqa_strided": ("const int64_t g = i / G;", "const int64_t g = i % j->n_kv_heads;"),
+    "scale_dropped": ("(double)kh[row * d + c];\n        z[s - lo] = acc * j->scale;",
+                      "(double)kh[row * d + c];\n        z[s - lo] = acc;"),
+    "exp_sign_flipped": ("int64_t row = s - j->hist_lo[b];\n        double w = exp(z[s - lo] - m);",
+                         "int64_t row = s - j->hist_lo[b];\n        double w = exp(m - z[s - lo]);"),
+    "gqa_strided": ("const int64_t g = i / G; /* query head i reads KV head floor(i/G) */\n    const int64_t t = j->pos[b];",
+                    "const int64_t g = i % j->n_kv_heads;\n    const int64_t t = j->pos[b];"),
     "value_operand_swapped": ("o[c] += w * (double)vh[row * d + c];",
                               "o[c] += w * (double)kh[row * d + c];"),
     "normalisation_dropped": ("(void)cnt;\n    for (int64_t c = 0; c < d; ++c) o[c] /= den;",
