@@ -159,6 +159,35 @@ pbb_status_t swa_decode_step_advance(const pbb_desc_t *desc, const int32_t *pos,
                                      void *k_ring, void *v_ring, void *out, void *workspace,
                                      size_t workspace_bytes, void *stream);
 
+/*
+ * Prefill: attention for every position of prompts at positions 0..n-1, the step that fills
+ * the cache before decoding (Sec. 3: one fused kernel over block tiles and bridge rectangles
+ * with log-sum-exp rescaling and native GQA; Appendix F.4: the added edges are h x h
+ * target-by-source rectangles, no dense mask).  For every sequence b, position t < n and query
+ * head i: out[b][t][i] = softmax over s in A_PBB(t) of (q[b][t][i] . k[b][s][floor(i/G)] *
+ * scale) applied to v[b][s][floor(i/G)] (Eq.(pbb) with h = B/2, Eq.(attention)).
+ *   q, out   [batch][n][n_q_heads][head_dim]   (token-major, as projections produce them)
+ *   k, v     [batch][n][n_kv_heads][head_dim]
+ *   lse      optional float32 [batch][n_q_heads][n]: log sum_{s in A(t)} e^{z_s}, natural log
+ *            (the log-partition of Appendix A.4, Eq.(lse)); NULL skips it
+ *   k_ring, v_ring  optional (both or neither), [batch][n_kv_heads][slots][head_dim]: every
+ *            slot j that some position s in max(0, n - slots)..n-1 maps to (j = s mod slots)
+ *            receives k/v of the last such s; other slots are left as they are.  After
+ *            pbb_ring_init and this call, decoding continues with pos[b] = n (Appendix F.1).
+ * bfloat16 only (PBB_ERR_DTYPE otherwise); fp32 accumulation, output rounded RNE.  Requires
+ * 0 <= n <= 2^30; n == 0 does nothing.  q, k, v, out, rings 16-byte aligned, lse 4-byte
+ * aligned.  Same descriptor rules as pbb_decode_step; no workspace.
+ */
+pbb_status_t pbb_prefill(const pbb_desc_t *desc, int32_t n, const void *q, const void *k,
+                         const void *v, void *out, float *lse, void *k_ring, void *v_ring,
+                         void *stream);
+
+/* Sliding-window prefill with the same arguments: support {max(0, t-W+1) .. t} (Prop. 2),
+ * W = desc->window, ring of desc->slots >= W entries (SWA descriptor rules). */
+pbb_status_t swa_prefill(const pbb_desc_t *desc, int32_t n, const void *q, const void *k,
+                         const void *v, void *out, float *lse, void *k_ring, void *v_ring,
+                         void *stream);
+
 #ifdef __cplusplus
 }
 #endif

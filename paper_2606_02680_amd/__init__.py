@@ -5,5 +5,5 @@ The product is ``libpbb.so`` (C ABI in ``include/pbb.h``, HIP kernels for gfx950
 """
 from .pbb import (  # noqa: F401
     PbbDesc, PbbError, alloc_rings, alloc_workspace, load_library, make_desc, pbb_decode_step,
-    pbb_decode_step_advance, ring_bytes, ring_fill, ring_init, swa_decode_step,
-    swa_decode_step_advance, swa_workspace_bytes, workspace_bytes)
+    pbb_decode_step_advance, pbb_prefill, ring_bytes, ring_fill, ring_init, swa_decode_step,
+    swa_decode_step_advance, swa_prefill, swa_workspace_bytes, workspace_bytes)

@@ -15,6 +15,7 @@ namespace {
 
 constexpr int32_t kMaxGroup = 16;     // query heads per KV head held by one MFMA tile
 constexpr int32_t kMaxSlots = 65536;  // ring slots per (sequence, KV head)
+constexpr int32_t kMaxPrefill = 1 << 30;  // prompt positions per call
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
@@ -90,6 +91,48 @@ pbb_status_t decode_common(const pbb_desc_t* desc, bool swa, const int32_t* pos,
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   const hipError_t e = desc->dtype == PBB_DTYPE_BF16 ? pbb::launch_decode_bf16(a, desc->head_dim, s)
                                                      : pbb::launch_decode_f32(a, desc->head_dim, s);
+  return e == hipSuccess ? PBB_OK : PBB_ERR_LAUNCH;
+}
+
+pbb_status_t prefill_common(const pbb_desc_t* desc, bool swa, int32_t n, const void* q,
+                            const void* k, const void* v, void* out, float* lse, void* k_ring,
+                            void* v_ring, void* stream) {
+  const pbb_status_t st = check_desc(desc, swa);
+  if (st != PBB_OK) return st;
+  if (desc->dtype != PBB_DTYPE_BF16) return PBB_ERR_DTYPE;
+  if (n < 0 || n > kMaxPrefill) return PBB_ERR_SHAPE;
+  if (!q || !k || !v || !out) return PBB_ERR_NULL;
+  if ((k_ring == nullptr) != (v_ring == nullptr)) return PBB_ERR_NULL;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16) ||
+      !aligned(k_ring, 16) || !aligned(v_ring, 16) || !aligned(lse, 4))
+    return PBB_ERR_ALIGN;
+  // Workgroups: one per (sequence, KV head, tile of at least 8 positions).
+  if ((uint64_t)desc->batch * (uint64_t)desc->n_kv_heads * ((uint64_t)n / 8 + 1) > 0x7fffffffull)
+    return PBB_ERR_SHAPE;
+  if (n == 0) return PBB_OK;
+
+  pbb::PrefillArgs a;
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.out = out;
+  a.lse = lse;
+  a.k_ring = k_ring;
+  a.v_ring = v_ring;
+  a.batch = desc->batch;
+  a.n = n;
+  a.hq = desc->n_q_heads;
+  a.hkv = desc->n_kv_heads;
+  a.group = desc->n_q_heads / desc->n_kv_heads;
+  a.mode = swa ? pbb::kSupportSWA : pbb::kSupportPBB;
+  a.block = desc->block;
+  a.window = desc->window;
+  a.slots = desc->slots;
+  const float scale = desc->scale > 0.0f ? desc->scale
+                                         : (float)(1.0 / std::sqrt((double)desc->head_dim));
+  a.scale_log2 = (float)((double)scale * 1.4426950408889634);  // log2(e)
+  const hipError_t e =
+      pbb::launch_prefill_bf16(a, desc->head_dim, reinterpret_cast<hipStream_t>(stream));
   return e == hipSuccess ? PBB_OK : PBB_ERR_LAUNCH;
 }
 
@@ -190,6 +233,18 @@ pbb_status_t swa_decode_step_advance(const pbb_desc_t* desc, const int32_t* pos,
                                      size_t workspace_bytes, void* stream) {
   return decode_common(desc, true, pos, pos_next, true, q, k_new, v_new, k_ring, v_ring, out,
                        workspace, workspace_bytes, stream);
+}
+
+pbb_status_t pbb_prefill(const pbb_desc_t* desc, int32_t n, const void* q, const void* k,
+                         const void* v, void* out, float* lse, void* k_ring, void* v_ring,
+                         void* stream) {
+  return prefill_common(desc, false, n, q, k, v, out, lse, k_ring, v_ring, stream);
+}
+
+pbb_status_t swa_prefill(const pbb_desc_t* desc, int32_t n, const void* q, const void* k,
+                         const void* v, void* out, float* lse, void* k_ring, void* v_ring,
+                         void* stream) {
+  return prefill_common(desc, true, n, q, k, v, out, lse, k_ring, v_ring, stream);
 }
 
 }  // extern "C"

@@ -31,6 +31,27 @@ struct DecodeArgs {
   float scale_log2;    // softmax scale times log2(e)
 };
 
+// Prefill of prompts at positions 0..n-1, validated on the host before launch.
+struct PrefillArgs {
+  const void* q;       // [batch][n][hq][d]
+  const void* k;       // [batch][n][hkv][d]
+  const void* v;
+  void* out;           // [batch][n][hq][d]
+  float* lse;          // optional [batch][hq][n]
+  void* k_ring;        // optional [batch][hkv][slots][d]
+  void* v_ring;
+  int32_t batch;
+  int32_t n;
+  int32_t hq;
+  int32_t hkv;
+  int32_t group;
+  int32_t mode;        // SupportMode
+  int32_t block;
+  int32_t window;
+  int32_t slots;
+  float scale_log2;
+};
+
 hipError_t launch_ring_zero(void* k_ring, void* v_ring, size_t bytes_per_tensor,
                             hipStream_t stream);
 
@@ -41,6 +62,9 @@ hipError_t launch_ring_fill(const int32_t* pos, const void* k_src, const void* v
 
 // bf16 decode on matrix cores; head_dim 64 or 128.
 hipError_t launch_decode_bf16(const DecodeArgs& a, int32_t head_dim, hipStream_t stream);
+
+// bf16 prefill on matrix cores; head_dim 64 or 128; n >= 1.
+hipError_t launch_prefill_bf16(const PrefillArgs& a, int32_t head_dim, hipStream_t stream);
 
 // fp32 decode on vector ALUs; head_dim 64 or 128.
 hipError_t launch_decode_f32(const DecodeArgs& a, int32_t head_dim, hipStream_t stream);

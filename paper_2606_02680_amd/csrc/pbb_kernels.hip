@@ -20,19 +20,11 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "pbb_device.h"
 #include "pbb_internal.h"
 
 namespace pbb {
 namespace {
-
-typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
-typedef __attribute__((ext_vector_type(4))) float f32x4;
-typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
-
-// Cache-policy operand of global_load_lds selecting the non-temporal ("nt") hint.
-constexpr int kCachePolicyNT = 2;
-
-constexpr float kNegInf = -__builtin_huge_valf();
 
 // Ring-key ranges of one (sequence, KV head) at position t.
 struct Ranges {
@@ -72,15 +64,6 @@ __device__ __forceinline__ Ranges ranges_for(const DecodeArgs& a, int t) {
 __device__ __forceinline__ int ring_slot(const Ranges& R, int i) {
   return i < R.len0 ? R.base0 + i : i - R.len0;
 }
-
-// float -> bf16 with round-to-nearest-even (inputs are finite).
-__device__ __forceinline__ uint16_t float_to_bf16_rne(float f) {
-  uint32_t u = __float_as_uint(f);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
-}
-
-__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // ------------------------------------------------------------------------------------------
 // Ring maintenance

@@ -1,0 +1,293 @@
+// HIP prefill kernel for Post-Boundary Bridge (PBB) attention on gfx950 (MI355X, CDNA4).
+//
+// Every position t = 0..n-1 of a prompt attends with one softmax over its own support
+// (Sec. 3, Eq.(pbb) and Eq.(attention)).  With h = B/2 that support is the interval
+// [a(t), t], a(t) = max(0, h*(floor(t/h) - 1)) (Sec. 3 "Flash-PBB"; Appendix A.3): the causal
+// block prefix plus, for the first h phases of a block, the preceding half-block, i.e. causal
+// block tiles plus h x h bridge rectangles (Appendix F.4), never a dense n x n mask.  The
+// sliding-window variant uses [max(0, t-W+1), t] (Prop. 2).  a(t) never decreases, so the
+// keys any run of consecutive positions needs form one interval.
+//
+// Work unit: TQ = floor(16*QC*NW / G) consecutive positions of one (sequence, KV head) with
+// all G query heads of that KV head, i.e. 16*QC*NW query columns ordered position-major,
+// head-minor (native grouped-query attention: the K/V tile is read once for the group).
+// Keys of the unit's interval stream through LDS in 32-key steps, three stages deep, each
+// tile loaded once per workgroup by LDS DMA and shared by the 4 waves; each wave owns QC
+// groups of 16 columns.  Per step a wave computes S^T = K Q^T and O^T += V^T P^T on
+// v_mfma_f32_16x16x32_bf16 exactly as the decode kernel does, the 16 B-operand columns being
+// 16 queries; per-column bounds mask the tile; the online softmax keeps fp32 running
+// maxima and sums (the log-sum-exp rescaling of Appendix A.4, Eq.(lse)).  Outputs are rounded
+// to bf16 (RNE); the log-partition is written in natural-log units.  Finally every workgroup
+// copies those of its positions that fall in the last `slots` positions of the prompt into the
+// ring (slot s mod slots, Appendix F.1), the state decode continues from.
+
+#include "pbb_device.h"
+#include "pbb_internal.h"
+
+namespace pbb {
+namespace {
+
+constexpr int kPrefillWaves = 4;
+constexpr int kPrefillColGroups = 2;   // 16-column groups per wave
+constexpr int kPrefillCols = 16 * kPrefillColGroups * kPrefillWaves;
+
+__device__ __forceinline__ int support_lo(const PrefillArgs& a, int t) {
+  if (a.mode == kSupportPBB) {
+    const int h = a.block >> 1;
+    const int lo = h * (t / h - 1);
+    return lo > 0 ? lo : 0;
+  }
+  const int lo = t - a.window + 1;
+  return lo > 0 ? lo : 0;
+}
+
+template <int D, int QC>
+__global__ __launch_bounds__(kPrefillWaves * 64) void prefill_bf16_kernel(PrefillArgs a,
+                                                                          int tq, int tiles) {
+  constexpr int NW = kPrefillWaves;
+  constexpr int KK = D / 32;            // 32-channel slices of the score contraction
+  constexpr int NB = D / 16;            // 16-channel blocks of the output
+  constexpr int ROWB = D * 2;           // bytes of one K or V row
+  constexpr int PPR = D / 8;            // 16-byte pieces per row
+  constexpr int RPI = 64 / PPR;         // rows per 1 KiB DMA group
+  constexpr int NG = 32 / RPI;          // DMA groups per step and tensor
+  constexpr int VPITCH = 1024 + (D == 128 ? 32 : 64);
+  constexpr int KTILE = 32 * ROWB;
+  constexpr int VTILE = NG * VPITCH;
+  constexpr int BUF = KTILE + VTILE;
+  constexpr int STAGES = 3;
+  constexpr int OPS = 2 * NG;           // DMA instructions per step (K tile, then V tile)
+  constexpr int MYOPS = OPS / NW;       // issued by each wave
+  static_assert(OPS % NW == 0, "DMA split");
+  __shared__ __align__(16) unsigned char smem[STAGES * BUF];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int c16 = lane & 15;
+  const int j4 = lane >> 4;
+  const int G = a.group;
+  const int n = a.n;
+
+  // Workgroup i runs on XCD i mod 8; give each XCD a contiguous run of tiles so that tiles
+  // sharing keys (neighbours of one sequence and KV head) share that XCD's L2.
+  const int nblk = gridDim.x;
+  const int per = nblk >> 3, rem = nblk & 7;
+  const int xcd = blockIdx.x & 7, local = blockIdx.x >> 3;
+  const int tile_id = (xcd < rem ? xcd * (per + 1) : rem * (per + 1) + (xcd - rem) * per) + local;
+  const int bg = tile_id / tiles;
+  const int tile = tile_id - bg * tiles;
+  const int b = bg / a.hkv;
+  const int g = bg - b * a.hkv;
+  const int t0 = tile * tq;
+  const int t_last = min(n - 1, t0 + tq - 1);
+  const int kbeg = support_lo(a, t0);
+  const int s_first = kbeg >> 5;
+  const int nsteps = (t_last >> 5) - s_first + 1;
+
+  const size_t rowstride = (size_t)a.hkv * ROWB;  // bytes between consecutive positions
+  const unsigned char* kbase = (const unsigned char*)a.k + ((size_t)b * n * a.hkv + g) * ROWB;
+  const unsigned char* vbase = (const unsigned char*)a.v + ((size_t)b * n * a.hkv + g) * ROWB;
+
+  // This lane's query columns: column c -> position t0 + c / G, head g*G + c % G.
+  int lo_c[QC], hi_c[QC], tcol[QC], hcol[QC];
+  bool valid[QC];
+  bf16x8 qB[QC][KK];
+#pragma unroll
+  for (int qc = 0; qc < QC; ++qc) {
+    const int col = (wave * QC + qc) * 16 + c16;
+    const int cp = col / G;
+    tcol[qc] = t0 + cp;
+    hcol[qc] = g * G + (col - cp * G);
+    valid[qc] = cp < tq && tcol[qc] < n;
+    lo_c[qc] = valid[qc] ? support_lo(a, tcol[qc]) : 0x7fffffff;
+    hi_c[qc] = valid[qc] ? tcol[qc] : -1;
+    const uint16_t* qrow = (const uint16_t*)a.q +
+        ((size_t)(b * (size_t)n + (valid[qc] ? tcol[qc] : t0)) * a.hq + hcol[qc]) * D;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      const u32x4 w = *(const u32x4*)(qrow + 32 * kk + 8 * j4);
+      const u32x4 zero = {0u, 0u, 0u, 0u};
+      qB[qc][kk] = __builtin_bit_cast(bf16x8, valid[qc] ? w : zero);
+    }
+  }
+
+  auto swz_k = [](int r) -> int { return D == 128 ? (r & 15) : ((r >> 1) & 7); };
+  auto swz_v = [](int rr) -> int { return (D == 64 && rr >= 4) ? 2 : 0; };
+
+  // This wave's share of the DMA of step st (keys 32*(s_first + st) ..), into stage `stage`.
+  // Keys past t_last are clamped to t_last (read, then masked for every column).
+  auto issue = [&](int stage, int st) {
+    unsigned char* tile_p = smem + stage * BUF;
+    const int k0 = (s_first + st) * 32;
+    const int rr = lane / PPR;
+    const int pc = lane % PPR;
+#pragma unroll
+    for (int o = 0; o < MYOPS; ++o) {
+      const int op = wave * MYOPS + o;
+      const bool isv = op >= NG;
+      const int x = isv ? op - NG : op;
+      const int row = x * RPI + rr;
+      const int key = min(k0 + row, t_last);
+      const int piece = pc ^ (isv ? swz_v(rr) : swz_k(row));
+      const unsigned char* src = (isv ? vbase : kbase) + (size_t)key * rowstride + piece * 16;
+      unsigned char* dst = tile_p + (isv ? KTILE + x * VPITCH : x * 1024);
+      __builtin_amdgcn_global_load_lds((const void*)src,
+                                       (__attribute__((address_space(3))) void*)dst, 16, 0, 0);
+    }
+  };
+
+  float m[QC], lsum[QC];
+  f32x4 acc[QC][NB];
+#pragma unroll
+  for (int qc = 0; qc < QC; ++qc) {
+    m[qc] = kNegInf;
+    lsum[qc] = 0.0f;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) acc[qc][nb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+  }
+
+  issue(0, 0);
+  if (nsteps > 1) issue(1, 1);
+
+  for (int st = 0; st < nsteps; ++st) {
+    // This wave's loads of step st have landed once at most step st+1's are outstanding; the
+    // barrier then covers every wave's loads, and every wave is done with step st-1, whose
+    // stage the loads of step st+2 reuse.
+    if (st + 1 < nsteps)
+      __builtin_amdgcn_s_waitcnt(0x0F70 | (MYOPS & 15) | ((MYOPS >> 4) << 14));
+    else
+      __builtin_amdgcn_s_waitcnt(0x0F70);
+    lds_barrier();
+    if (st + 2 < nsteps) issue((st + 2) % STAGES, st + 2);
+    __builtin_amdgcn_sched_barrier(0);
+
+    const unsigned char* tile_p = smem + (st % STAGES) * BUF;
+    const int k0 = (s_first + st) * 32;
+    f32x4 s0[QC], s1[QC];
+#pragma unroll
+    for (int qc = 0; qc < QC; ++qc) {
+      s0[qc] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+      s1[qc] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    }
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      const int p = 4 * kk + j4;
+      const bf16x8 ka = *(const bf16x8*)(tile_p + c16 * ROWB + ((p ^ swz_k(c16)) << 4));
+      const bf16x8 kb =
+          *(const bf16x8*)(tile_p + (16 + c16) * ROWB + ((p ^ swz_k(16 + c16)) << 4));
+#pragma unroll
+      for (int qc = 0; qc < QC; ++qc) {
+        s0[qc] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qB[qc][kk], s0[qc], 0, 0, 0);
+        s1[qc] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb, qB[qc][kk], s1[qc], 0, 0, 0);
+      }
+    }
+    bf16x8 pB[QC];
+    float alpha[QC];
+#pragma unroll
+    for (int qc = 0; qc < QC; ++qc) {
+      float z[8];
+      float mx = kNegInf;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int key = k0 + (e < 4 ? 4 * j4 + e : 16 + 4 * j4 + (e - 4));
+        const float sc = (e < 4 ? s0[qc][e] : s1[qc][e - 4]) * a.scale_log2;
+        z[e] = (key >= lo_c[qc] && key <= hi_c[qc]) ? sc : kNegInf;
+        mx = fmaxf(mx, z[e]);
+      }
+      mx = fmaxf(mx, __shfl_xor(mx, 16));
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float mn = fmaxf(m[qc], mx);
+      const float ms = mn == kNegInf ? 0.0f : mn;  // a column with no key yet stays empty
+      alpha[qc] = fast_exp2(m[qc] - ms);
+      float ps = 0.0f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float pe = fast_exp2(z[e] - ms);
+        ps += pe;
+        pB[qc][e] = (__bf16)pe;
+      }
+      lsum[qc] = lsum[qc] * alpha[qc] + ps;
+      m[qc] = mn;
+    }
+    const unsigned char* vt = tile_p + KTILE;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      const int colv = 16 * nb + c16;
+      bf16x8 va;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int row = e < 4 ? 4 * j4 + e : 16 + 4 * j4 + (e - 4);
+        const int rr = row % RPI;
+        const int off = (row / RPI) * VPITCH + rr * ROWB + (((colv >> 3) ^ swz_v(rr)) << 4) +
+                        ((colv & 7) << 1);
+        va[e] = *(const __bf16*)(vt + off);
+      }
+#pragma unroll
+      for (int qc = 0; qc < QC; ++qc) {
+        acc[qc][nb] *= alpha[qc];
+        acc[qc][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pB[qc], acc[qc][nb], 0, 0, 0);
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+
+  // Outputs: o = acc / l (bf16 RNE), lse = (m + log2 l) * ln 2.
+#pragma unroll
+  for (int qc = 0; qc < QC; ++qc) {
+    float l = lsum[qc];
+    l += __shfl_xor(l, 16);
+    l += __shfl_xor(l, 32);
+    if (!valid[qc]) continue;
+    const float inv = 1.0f / l;
+    uint16_t* orow = (uint16_t*)a.out + ((size_t)(b * (size_t)n + tcol[qc]) * a.hq + hcol[qc]) * D;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      u32x2 w;
+      w[0] = (uint32_t)float_to_bf16_rne(acc[qc][nb][0] * inv) |
+             ((uint32_t)float_to_bf16_rne(acc[qc][nb][1] * inv) << 16);
+      w[1] = (uint32_t)float_to_bf16_rne(acc[qc][nb][2] * inv) |
+             ((uint32_t)float_to_bf16_rne(acc[qc][nb][3] * inv) << 16);
+      *(u32x2*)(orow + 16 * nb + 4 * j4) = w;
+    }
+    if (a.lse != nullptr && j4 == 0)
+      a.lse[((size_t)b * a.hq + hcol[qc]) * n + tcol[qc]] =
+          (m[qc] + __builtin_log2f(l)) * 0.69314718055994531f;
+  }
+
+  // Ring state after the prompt: positions max(0, n - slots) .. n-1 at slot s mod slots.
+  if (a.k_ring != nullptr) {
+    const int first = max(t0, n - a.slots);
+    const int count = t_last - first + 1;
+    for (int idx = tid; idx < 2 * count * PPR; idx += NW * 64) {
+      const int which = idx / (count * PPR);
+      const int rest = idx - which * count * PPR;
+      const int t = first + rest / PPR;
+      const int pc = rest % PPR;
+      const unsigned char* src = (which ? vbase : kbase) + (size_t)t * rowstride + pc * 16;
+      unsigned char* dst = (unsigned char*)(which ? a.v_ring : a.k_ring) +
+                           ((size_t)bg * a.slots + (t % a.slots)) * ROWB + pc * 16;
+      *(u32x4*)dst = *(const u32x4*)src;
+    }
+  }
+}
+
+template <int D>
+hipError_t launch_prefill_d(const PrefillArgs& a, hipStream_t stream) {
+  const int tq = kPrefillCols / a.group;
+  const int tiles = (a.n + tq - 1) / tq;
+  const size_t blocks = (size_t)a.batch * a.hkv * tiles;
+  if (blocks == 0) return hipSuccess;
+  if (blocks > 0x7fffffffull) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((prefill_bf16_kernel<D, kPrefillColGroups>), dim3((unsigned)blocks),
+                     dim3(kPrefillWaves * 64), 0, stream, a, tq, tiles);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_prefill_bf16(const PrefillArgs& a, int32_t head_dim, hipStream_t stream) {
+  return head_dim == 128 ? launch_prefill_d<128>(a, stream) : launch_prefill_d<64>(a, stream);
+}
+
+}  // namespace pbb

@@ -24,7 +24,7 @@ _TORCH_DTYPE = {DTYPE_F32: torch.float32, DTYPE_BF16: torch.bfloat16}
 
 EXPORTS = ("pbb_status_string", "pbb_ring_bytes", "pbb_ring_init", "pbb_ring_fill",
            "pbb_workspace_bytes", "pbb_decode_step", "swa_workspace_bytes", "swa_decode_step",
-           "pbb_decode_step_advance", "swa_decode_step_advance")
+           "pbb_decode_step_advance", "swa_decode_step_advance", "pbb_prefill", "swa_prefill")
 
 
 class PbbError(RuntimeError):
@@ -74,6 +74,8 @@ def load_library(path: str = _LIB_PATH):
         getattr(lib, fn).argtypes = [dp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     for fn in ("pbb_decode_step_advance", "swa_decode_step_advance"):
         getattr(lib, fn).argtypes = [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    for fn in ("pbb_prefill", "swa_prefill"):
+        getattr(lib, fn).argtypes = [dp, i32, vp, vp, vp, vp, vp, vp, vp, vp]
     for fn in EXPORTS[1:]:
         getattr(lib, fn).restype = ctypes.c_int
     _lib = lib
@@ -229,6 +231,39 @@ def swa_decode_step_advance(desc: PbbDesc, pos, pos_next, q, k_new, v_new, k_rin
     """:func:`swa_decode_step` that also writes ``pos_next = pos + 1`` (``pos`` unchanged)."""
     return _decode("swa_decode_step_advance", desc, pos, q, k_new, v_new, k_ring, v_ring, out,
                    workspace, stream, pos_next=pos_next)
+
+
+def _prefill(fn: str, desc: PbbDesc, q, k, v, out, lse, k_ring, v_ring, stream):
+    if q.dim() != 4:
+        raise ValueError(f"{fn}: q must be [batch][n][Hq][d], got {tuple(q.shape)}")
+    n = q.shape[1]
+    _expect("q", q, (desc.batch, n, desc.n_q_heads, desc.head_dim), desc.torch_dtype)
+    _expect("out", out, (desc.batch, n, desc.n_q_heads, desc.head_dim), desc.torch_dtype)
+    for name, t in (("k", k), ("v", v)):
+        _expect(name, t, (desc.batch, n, desc.n_kv_heads, desc.head_dim), desc.torch_dtype)
+    if lse is not None:
+        _expect("lse", lse, (desc.batch, desc.n_q_heads, n), torch.float32)
+    if (k_ring is None) != (v_ring is None):
+        raise ValueError(f"{fn}: pass both rings or neither")
+    if k_ring is not None:
+        for name, t in (("k_ring", k_ring), ("v_ring", v_ring)):
+            _expect(name, t, ring_shape(desc), desc.torch_dtype)
+    _check(fn, getattr(load_library(), fn)(
+        ctypes.byref(desc), int(n), _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse),
+        _ptr(k_ring), _ptr(v_ring), _stream(stream)))
+    return out
+
+
+def pbb_prefill(desc: PbbDesc, q, k, v, out, lse=None, k_ring=None, v_ring=None, stream=None):
+    """PBB attention for every position of prompts at positions ``0 .. n-1`` (q, out
+    [batch][n][Hq][d]; k, v [batch][n][Hkv][d]); optional log-partitions ``lse``
+    [batch][Hq][n] (float32) and ring state for decoding from position ``n``."""
+    return _prefill("pbb_prefill", desc, q, k, v, out, lse, k_ring, v_ring, stream)
+
+
+def swa_prefill(desc: PbbDesc, q, k, v, out, lse=None, k_ring=None, v_ring=None, stream=None):
+    """Sliding-window counterpart of :func:`pbb_prefill` (support of Prop. 2)."""
+    return _prefill("swa_prefill", desc, q, k, v, out, lse, k_ring, v_ring, stream)
 
 
 def default_scale(head_dim: int) -> float:

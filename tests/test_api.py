@@ -174,3 +174,37 @@ def test_failed_calls_leave_buffers_untouched(cuda):
     P.pbb_decode_step(desc, pos, q.zero_(), kn.zero_(), vn.zero_(), kr.zero_(), vr.zero_(), out)
     torch.cuda.synchronize()
     assert not bool((out.view(torch.int16) == canary).any())
+
+
+def _prefill(desc, fn="pbb_prefill", n=64, **ptrs):
+    args = dict(q=A, k=A, v=A, out=A, lse=0, kr=0, vr=0)
+    args.update(ptrs)
+    vp = ctypes.c_void_p
+    return getattr(B.load_library(), fn)(
+        ctypes.byref(desc), n, vp(args["q"]), vp(args["k"]), vp(args["v"]), vp(args["out"]),
+        vp(args["lse"]), vp(args["kr"]), vp(args["vr"]), vp(0))
+
+
+@pytest.mark.parametrize("fn", ["pbb_prefill", "swa_prefill"])
+def test_prefill_argument_errors(fn):
+    desc = _desc(window=32, slots=64) if fn == "swa_prefill" else _desc()
+    lib = B.load_library()
+    vp = ctypes.c_void_p
+    assert getattr(lib, fn)(None, 8, vp(A), vp(A), vp(A), vp(A), vp(0), vp(0), vp(0), vp(0)) == 1
+    for name in ("q", "k", "v", "out"):
+        assert _prefill(desc, fn, **{name: 0}) == 1, name
+    assert _prefill(desc, fn, kr=A) == 1                 # one ring without the other
+    assert _prefill(desc, fn, vr=A) == 1
+    assert _prefill(desc, fn, n=-1) == 2
+    assert _prefill(desc, fn, n=(1 << 30) + 1) == 2
+    for name in ("q", "k", "v", "out", "kr"):
+        kw = {name: A + 8}
+        if name == "kr":
+            kw["vr"] = A
+        assert _prefill(desc, fn, **kw) == 4, name
+    assert _prefill(desc, fn, lse=A + 2) == 4
+    f32 = _desc(window=32, slots=64, dtype=B.DTYPE_F32) if fn == "swa_prefill" else _desc(dtype=B.DTYPE_F32)
+    assert _prefill(f32, fn) == 3                         # bf16 only
+    bad = _desc(window=65, slots=64) if fn == "swa_prefill" else _desc(block=63, slots=63)
+    assert _prefill(bad, fn) == 2
+    assert _prefill(desc, fn, n=0) == 0                   # nothing to do, nothing launched

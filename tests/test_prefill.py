@@ -1,0 +1,140 @@
+"""GPU parity of the prefill entry points (``pbb_prefill``, ``swa_prefill``) against the fp64
+oracle, through the C ABI.
+
+Every position of every sequence is compared: outputs at the bf16 tolerance of the decode
+tests, log-partitions within 2e-3 (fp32 running sums of the same bf16 inputs); ring state
+after the prompt bit for bit (slot s mod slots holds the last prompt position s); and
+decoding continued from that ring at position n matches the oracle over prompt plus new
+tokens.  Shapes cover group sizes 1..16 including ones that do not divide the 128-column tile
+(5, 6, 7), both head dims, blocks from 2 to 2048, prompts shorter than one tile and ragged
+tails, and the sliding window.
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2606_02680_amd as P
+import workloads as W
+from tests.harness import bits, compare, to_np
+
+pytestmark = pytest.mark.gpu
+
+
+def _cfg(mode, batch, n, hq, hkv, d, block=0, window=0, slots=0, seed=31, scale=1.0):
+    return W.Config(f"prefill-{mode}-{batch}-{n}-{hq}-{hkv}-{d}-{block}-{window}", mode,
+                    batch=batch, hq=hq, hkv=hkv, d=d, block=block,
+                    slots=slots or (block if mode == "pbb" else window), window=window,
+                    dtype="bf16", seed=seed, value_scale=scale, pos_hi=0, steps=n)
+
+
+def _desc(cfg):
+    if cfg.mode == "swa":
+        return P.make_desc(cfg.batch, cfg.hq, cfg.hkv, cfg.d, window=cfg.window, slots=cfg.slots,
+                           dtype=torch.bfloat16)
+    return P.make_desc(cfg.batch, cfg.hq, cfg.hkv, cfg.d, block=cfg.block, dtype=torch.bfloat16)
+
+
+def _run(cfg, n, device, rings=True):
+    q, k, v = W.prompt(cfg, n, device=device)
+    desc = _desc(cfg)
+    out = torch.full_like(q, float("nan"))
+    lse = torch.full((cfg.batch, cfg.hq, n), float("nan"), dtype=torch.float32, device=device)
+    kr = vr = None
+    if rings:
+        kr, vr = P.alloc_rings(desc, device)
+        P.ring_init(desc, kr, vr)
+    fn = P.swa_prefill if cfg.mode == "swa" else P.pbb_prefill
+    print(f"[prefill] {cfg.name}", flush=True)
+    fn(desc, q, k, v, out, lse, kr, vr)
+    torch.cuda.synchronize()
+    return desc, (q, k, v), out, lse, kr, vr
+
+
+def _check(cfg, n, device, rings=True):
+    desc, (q, k, v), out, lse, kr, vr = _run(cfg, n, device, rings)
+    mode = oracle.SWA if cfg.mode == "swa" else oracle.PBB
+    ref, ref_lse = oracle.prefill(mode, to_np(q), to_np(k), to_np(v), block=cfg.block,
+                                  window=cfg.window)
+    compare(cfg, to_np(out), ref, what=cfg.name)
+    got_lse = lse.cpu().numpy().astype(np.float64)
+    assert np.isfinite(got_lse).all()
+    assert np.abs(got_lse - ref_lse).max() <= 2e-3, np.abs(got_lse - ref_lse).max()
+    if rings:
+        kh = k.permute(0, 2, 1, 3).contiguous().cpu()
+        vh = v.permute(0, 2, 1, 3).contiguous().cpu()
+        zeros = np.zeros(kr.shape, dtype=np.int16)
+        for name, hist, ring in (("k", kh, kr), ("v", vh, vr)):
+            exp = oracle.expected_ring(bits(hist), np.zeros(cfg.batch), np.full(cfg.batch, n - 1),
+                                       np.zeros(cfg.batch), desc.slots, initial=zeros)
+            assert np.array_equal(bits(ring), exp), f"{cfg.name} ring {name}"
+    return desc, (q, k, v), out, lse, kr, vr
+
+
+@pytest.mark.parametrize("mode,batch,n,hq,hkv,d,block,window,slots", [
+    ("pbb", 2, 300, 8, 2, 64, 64, 0, 0),         # G = 4, several blocks, ragged tail
+    ("pbb", 1, 600, 12, 2, 64, 128, 0, 0),       # paper shape, G = 6 (21 positions / tile)
+    ("pbb", 1, 257, 10, 2, 64, 128, 0, 0),       # G = 5
+    ("pbb", 1, 200, 14, 2, 64, 128, 0, 0),       # G = 7
+    ("pbb", 2, 333, 32, 8, 128, 256, 0, 0),      # G = 4, head_dim 128
+    ("pbb", 1, 150, 16, 1, 128, 32, 0, 0),       # G = 16: 8 positions per tile
+    ("pbb", 1, 77, 4, 4, 64, 2, 0, 0),           # G = 1, B = 2 (h = 1)
+    ("pbb", 1, 5000, 8, 2, 128, 2048, 0, 0),     # long block, bridge rectangles of 1024
+    ("pbb", 3, 17, 6, 3, 64, 16, 0, 0),          # prompt shorter than one tile
+    ("pbb", 1, 1, 4, 1, 128, 64, 0, 0),          # a single position
+    ("swa", 2, 300, 8, 2, 128, 0, 100, 128),     # window 100 in 128 slots
+    ("swa", 1, 400, 6, 2, 64, 0, 37, 40),
+    ("swa", 1, 90, 4, 1, 64, 0, 1, 1),           # window 1: each position attends to itself
+])
+def test_prefill_matches_oracle(cuda, mode, batch, n, hq, hkv, d, block, window, slots):
+    cfg = _cfg(mode, batch, n, hq, hkv, d, block, window, slots)
+    _check(cfg, n, cuda)
+
+
+def test_prefill_without_optional_outputs(cuda):
+    cfg = _cfg("pbb", 1, 130, 8, 2, 64, 64)
+    q, k, v = W.prompt(cfg, 130, device=cuda)
+    desc = _desc(cfg)
+    out = torch.empty_like(q)
+    P.pbb_prefill(desc, q, k, v, out)
+    torch.cuda.synchronize()
+    ref, _ = oracle.prefill(oracle.PBB, to_np(q), to_np(k), to_np(v), block=64)
+    compare(cfg, to_np(out), ref, what="no lse, no rings")
+
+
+def test_prefill_then_decode_continues(cuda):
+    """Rings written by prefill are the state decode needs: steps at positions n, n+1, ...
+    match the oracle over prompt plus appended tokens."""
+    n, steps = 700, 70
+    cfg = _cfg("pbb", 2, n + steps, 8, 2, 128, 128)
+    desc, (q, k, v), out, lse, kr, vr = _run(cfg, n, cuda)
+    qa, ka, va = W.prompt(cfg, n + steps, device=cuda)   # positions 0 .. n+steps-1
+    pos = torch.full((cfg.batch,), n, dtype=torch.int32, device=cuda)
+    kh = ka.permute(0, 2, 1, 3).contiguous()
+    vh = va.permute(0, 2, 1, 3).contiguous()
+    for i in range(steps):
+        t = n + i
+        qd = qa[:, t].contiguous()
+        o = torch.empty_like(qd)
+        P.pbb_decode_step(desc, pos, qd, ka[:, t].contiguous(), va[:, t].contiguous(), kr, vr, o)
+        pos += 1
+        if i % 7 == 0 or i == steps - 1:
+            ref = oracle.decode(oracle.PBB, np.full(cfg.batch, t), to_np(qd), to_np(kh[:, :, :t + 1]),
+                                to_np(vh[:, :, :t + 1]), np.zeros(cfg.batch, np.int64), block=128)
+            compare(cfg, to_np(o), ref, what=f"decode after prefill, t={t}")
+
+
+def test_prefill_is_deterministic_and_leaves_inputs(cuda):
+    cfg = _cfg("pbb", 2, 260, 12, 2, 64, 128)
+    q, k, v = W.prompt(cfg, 260, device=cuda)
+    copies = [x.clone() for x in (q, k, v)]
+    desc = _desc(cfg)
+    o1, o2 = torch.empty_like(q), torch.empty_like(q)
+    P.pbb_prefill(desc, q, k, v, o1)
+    P.pbb_prefill(desc, q, k, v, o2)
+    torch.cuda.synchronize()
+    assert torch.equal(o1.view(torch.int16), o2.view(torch.int16))
+    for x, c in zip((q, k, v), copies):
+        assert torch.equal(x.view(torch.int16), c.view(torch.int16))

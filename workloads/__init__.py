@@ -6,4 +6,5 @@ HIP library consume the tensors it produces; neither of them imports it.
 """
 from .configs import CONFIGS, Config, get_config  # noqa: F401
 from .gen import (  # noqa: F401
-    hash_normal, kv_at, kv_steps, kv_window, q_at, q_steps, initial_positions, spike_mask)
+    hash_normal, kv_at, kv_steps, kv_window, prompt, q_at, q_steps, initial_positions,
+    spike_mask)

@@ -146,6 +146,19 @@ def q_at(cfg, pos: torch.Tensor, device="cpu") -> torch.Tensor:
     return x[:, :, 0, :].contiguous()
 
 
+def prompt(cfg, n: int, device="cpu"):
+    """Prompt tensors for positions ``0 .. n-1`` of every sequence, token-major:
+    ``q`` [batch][n][Hq][d] and ``k``, ``v`` [batch][n][Hkv][d].  Position ``s`` carries the
+    same values as decoding position ``s`` (``q_at``, ``kv_at``)."""
+    seq = torch.arange(cfg.batch, dtype=torch.int64)
+    pos = torch.arange(n, dtype=torch.int64).view(1, -1).expand(cfg.batch, n)
+    q = _normal_block(cfg, STREAM_Q, seq, cfg.hq, pos, device, False, 1 << 24)
+    k = kv_at(cfg, "k", seq, pos, device=device)
+    v = kv_at(cfg, "v", seq, pos, device=device)
+    return (q.permute(0, 2, 1, 3).contiguous(), k.permute(0, 2, 1, 3).contiguous(),
+            v.permute(0, 2, 1, 3).contiguous())
+
+
 def initial_positions(cfg) -> torch.Tensor:
     """int64 [batch] first decode position of every sequence (zeros, or U[0, pos_hi))."""
     if cfg.pos_hi <= 0:
