@@ -42,8 +42,8 @@ __device__ __forceinline__ int support_lo(const PrefillArgs& a, int t) {
 }
 
 template <int D, int QC>
-__global__ __launch_bounds__(kPrefillWaves * 64) void prefill_bf16_kernel(PrefillArgs a,
-                                                                          int tq, int tiles) {
+__global__ __launch_bounds__(kPrefillWaves * 64) __attribute__((amdgpu_waves_per_eu(2)))
+void prefill_bf16_kernel(PrefillArgs a, int tq, int tiles) {
   constexpr int NW = kPrefillWaves;
   constexpr int KK = D / 32;            // 32-channel slices of the score contraction
   constexpr int NB = D / 16;            // 16-channel blocks of the output
@@ -51,9 +51,8 @@ __global__ __launch_bounds__(kPrefillWaves * 64) void prefill_bf16_kernel(Prefil
   constexpr int PPR = D / 8;            // 16-byte pieces per row
   constexpr int RPI = 64 / PPR;         // rows per 1 KiB DMA group
   constexpr int NG = 32 / RPI;          // DMA groups per step and tensor
-  constexpr int VPITCH = 1024 + (D == 128 ? 32 : 64);
   constexpr int KTILE = 32 * ROWB;
-  constexpr int VTILE = NG * VPITCH;
+  constexpr int VTILE = 32 * ROWB;
   constexpr int BUF = KTILE + VTILE;
   constexpr int STAGES = 3;
   constexpr int OPS = 2 * NG;           // DMA instructions per step (K tile, then V tile)
@@ -84,6 +83,10 @@ __global__ __launch_bounds__(kPrefillWaves * 64) void prefill_bf16_kernel(Prefil
   const int kbeg = support_lo(a, t0);
   const int s_first = kbeg >> 5;
   const int nsteps = (t_last >> 5) - s_first + 1;
+  // Keys [mask_lo, mask_hi] are in the support of every position of the tile (a(t) never
+  // decreases): steps inside that range need no masking.
+  const int mask_lo = support_lo(a, t_last);
+  const int mask_hi = t0;
 
   const size_t rowstride = (size_t)a.hkv * ROWB;  // bytes between consecutive positions
   const unsigned char* kbase = (const unsigned char*)a.k + ((size_t)b * n * a.hkv + g) * ROWB;
@@ -113,7 +116,9 @@ __global__ __launch_bounds__(kPrefillWaves * 64) void prefill_bf16_kernel(Prefil
   }
 
   auto swz_k = [](int r) -> int { return D == 128 ? (r & 15) : ((r >> 1) & 7); };
-  auto swz_v = [](int rr) -> int { return (D == 64 && rr >= 4) ? 2 : 0; };
+  // V rows are stored whole, 32-byte chunk c of row r at chunk c ^ (r mod 4), so that the
+  // transposed reads below (4 rows x 32 bytes per 16 lanes) spread over all banks.
+  auto swz_v = [](int r) -> int { return 2 * (r & 3); };  // in 16-byte pieces
 
   // This wave's share of the DMA of step st (keys 32*(s_first + st) ..), into stage `stage`.
   // Keys past t_last are clamped to t_last (read, then masked for every column).
@@ -129,9 +134,9 @@ __global__ __launch_bounds__(kPrefillWaves * 64) void prefill_bf16_kernel(Prefil
       const int x = isv ? op - NG : op;
       const int row = x * RPI + rr;
       const int key = min(k0 + row, t_last);
-      const int piece = pc ^ (isv ? swz_v(rr) : swz_k(row));
+      const int piece = pc ^ (isv ? swz_v(row) : swz_k(row));
       const unsigned char* src = (isv ? vbase : kbase) + (size_t)key * rowstride + piece * 16;
-      unsigned char* dst = tile_p + (isv ? KTILE + x * VPITCH : x * 1024);
+      unsigned char* dst = tile_p + (isv ? KTILE : 0) + x * 1024;
       __builtin_amdgcn_global_load_lds((const void*)src,
                                        (__attribute__((address_space(3))) void*)dst, 16, 0, 0);
     }
@@ -164,6 +169,7 @@ __global__ __launch_bounds__(kPrefillWaves * 64) void prefill_bf16_kernel(Prefil
 
     const unsigned char* tile_p = smem + (st % STAGES) * BUF;
     const int k0 = (s_first + st) * 32;
+    const bool interior = k0 >= mask_lo && k0 + 31 <= mask_hi;
     f32x4 s0[QC], s1[QC];
 #pragma unroll
     for (int qc = 0; qc < QC; ++qc) {
@@ -190,9 +196,11 @@ __global__ __launch_bounds__(kPrefillWaves * 64) void prefill_bf16_kernel(Prefil
       float mx = kNegInf;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const int key = k0 + (e < 4 ? 4 * j4 + e : 16 + 4 * j4 + (e - 4));
-        const float sc = (e < 4 ? s0[qc][e] : s1[qc][e - 4]) * a.scale_log2;
-        z[e] = (key >= lo_c[qc] && key <= hi_c[qc]) ? sc : kNegInf;
+        z[e] = (e < 4 ? s0[qc][e] : s1[qc][e - 4]) * a.scale_log2;
+        if (!interior) {
+          const int key = k0 + (e < 4 ? 4 * j4 + e : 16 + 4 * j4 + (e - 4));
+          z[e] = (key >= lo_c[qc] && key <= hi_c[qc]) ? z[e] : kNegInf;
+        }
         mx = fmaxf(mx, z[e]);
       }
       mx = fmaxf(mx, __shfl_xor(mx, 16));
@@ -210,19 +218,24 @@ __global__ __launch_bounds__(kPrefillWaves * 64) void prefill_bf16_kernel(Prefil
       lsum[qc] = lsum[qc] * alpha[qc] + ps;
       m[qc] = mn;
     }
+    // V^T operand of O^T += V^T P^T: lane (c16, j4) needs channel 16nb + c16 of keys
+    // 4j4..4j4+3 and 16+4j4..16+4j4+3 (the key order of P^T in the score layout).  One
+    // transposed read per half: within each 16-lane group, lane i names 4 channels
+    // 16nb + 4(i mod 4) .. +3 of key row 4j4 + i/4, and lane c16 receives channel 16nb + c16 of
+    // those four rows.
     const unsigned char* vt = tile_p + KTILE;
+    const int vrow = 4 * j4 + (c16 >> 2);
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
-      const int colv = 16 * nb + c16;
-      bf16x8 va;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int row = e < 4 ? 4 * j4 + e : 16 + 4 * j4 + (e - 4);
-        const int rr = row % RPI;
-        const int off = (row / RPI) * VPITCH + rr * ROWB + (((colv >> 3) ^ swz_v(rr)) << 4) +
-                        ((colv & 7) << 1);
-        va[e] = *(const __bf16*)(vt + off);
-      }
+      const int off = (((nb ^ (c16 >> 2)) << 5) | ((c16 & 3) << 3));
+      typedef __attribute__((ext_vector_type(4))) short i16x4;
+      const i16x4 lo4 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (__attribute__((address_space(3))) i16x4*)(vt + vrow * ROWB + off));
+      const i16x4 hi4 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (__attribute__((address_space(3))) i16x4*)(vt + (vrow + 16) * ROWB + off));
+      const __attribute__((ext_vector_type(8))) short v8 = {lo4[0], lo4[1], lo4[2], lo4[3],
+                                                            hi4[0], hi4[1], hi4[2], hi4[3]};
+      const bf16x8 va = __builtin_bit_cast(bf16x8, v8);
 #pragma unroll
       for (int qc = 0; qc < QC; ++qc) {
         acc[qc][nb] *= alpha[qc];
