@@ -120,24 +120,37 @@ void prefill_bf16_kernel(PrefillArgs a, int tq, int tiles) {
   // transposed reads below (4 rows x 32 bytes per 16 lanes) spread over all banks.
   auto swz_v = [](int r) -> int { return 2 * (r & 3); };  // in 16-byte pieces
 
-  // This wave's share of the DMA of step st (keys 32*(s_first + st) ..), into stage `stage`.
-  // Keys past t_last are clamped to t_last (read, then masked for every column).
+  // This wave's share of the DMA of a step: MYOPS 1 KiB pieces, each lane one 16-byte piece of
+  // one key row.  Row pointers start at the first step and advance 32 rows per step; in the
+  // last step, keys past t_last are clamped to t_last (read, then masked for every column).
+  const unsigned char* src[MYOPS];
+  int row_of[MYOPS];
+#pragma unroll
+  for (int o = 0; o < MYOPS; ++o) {
+    const int op = wave * MYOPS + o;
+    const bool isv = op >= NG;
+    const int x = isv ? op - NG : op;
+    const int row = x * RPI + lane / PPR;
+    const int piece = (lane % PPR) ^ (isv ? swz_v(row) : swz_k(row));
+    row_of[o] = row;
+    src[o] = (isv ? vbase : kbase) + (size_t)(s_first * 32 + row) * rowstride + piece * 16;
+  }
+  const size_t step_bytes = 32 * rowstride;
   auto issue = [&](int stage, int st) {
     unsigned char* tile_p = smem + stage * BUF;
-    const int k0 = (s_first + st) * 32;
-    const int rr = lane / PPR;
-    const int pc = lane % PPR;
+    const bool tail = (s_first + st) * 32 + 31 > t_last;
 #pragma unroll
     for (int o = 0; o < MYOPS; ++o) {
       const int op = wave * MYOPS + o;
       const bool isv = op >= NG;
       const int x = isv ? op - NG : op;
-      const int row = x * RPI + rr;
-      const int key = min(k0 + row, t_last);
-      const int piece = pc ^ (isv ? swz_v(row) : swz_k(row));
-      const unsigned char* src = (isv ? vbase : kbase) + (size_t)key * rowstride + piece * 16;
+      const unsigned char* s = src[o] + (size_t)st * step_bytes;
+      if (tail) {
+        const int over = (s_first + st) * 32 + row_of[o] - t_last;
+        if (over > 0) s -= (size_t)over * rowstride;
+      }
       unsigned char* dst = tile_p + (isv ? KTILE : 0) + x * 1024;
-      __builtin_amdgcn_global_load_lds((const void*)src,
+      __builtin_amdgcn_global_load_lds((const void*)s,
                                        (__attribute__((address_space(3))) void*)dst, 16, 0, 0);
     }
   };
@@ -188,35 +201,55 @@ void prefill_bf16_kernel(PrefillArgs a, int tq, int tiles) {
         s1[qc] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb, qB[qc][kk], s1[qc], 0, 0, 0);
       }
     }
+    // Online softmax in log2 units with a lazily moved reference: m only moves (and the
+    // accumulators are rescaled) when some column's maximum exceeds it by more than 8, so that
+    // most steps skip the rescale and the weights stay <= 2^8.  The result is the same softmax:
+    // numerator and denominator share every reference change.
+    const float c = a.scale_log2;
     bf16x8 pB[QC];
     float alpha[QC];
+    bool grow_any = false;
 #pragma unroll
     for (int qc = 0; qc < QC; ++qc) {
-      float z[8];
       float mx = kNegInf;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        z[e] = (e < 4 ? s0[qc][e] : s1[qc][e - 4]) * a.scale_log2;
+        float sc = e < 4 ? s0[qc][e] : s1[qc][e - 4];
         if (!interior) {
           const int key = k0 + (e < 4 ? 4 * j4 + e : 16 + 4 * j4 + (e - 4));
-          z[e] = (key >= lo_c[qc] && key <= hi_c[qc]) ? z[e] : kNegInf;
+          sc = (key >= lo_c[qc] && key <= hi_c[qc]) ? sc : kNegInf;
+          if (e < 4) s0[qc][e] = sc; else s1[qc][e - 4] = sc;
         }
-        mx = fmaxf(mx, z[e]);
+        mx = fmaxf(mx, sc);
       }
       mx = fmaxf(mx, __shfl_xor(mx, 16));
       mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float mn = fmaxf(m[qc], mx);
-      const float ms = mn == kNegInf ? 0.0f : mn;  // a column with no key yet stays empty
-      alpha[qc] = fast_exp2(m[qc] - ms);
+      const float cand = mx * c;
+      const bool grow = cand > m[qc] + 8.0f;
+      alpha[qc] = grow ? fast_exp2(m[qc] - cand) : 1.0f;
+      m[qc] = grow ? cand : m[qc];
+      grow_any |= grow;
+    }
+    if (__builtin_amdgcn_ballot_w64(grow_any) != 0) {
+#pragma unroll
+      for (int qc = 0; qc < QC; ++qc) {
+        lsum[qc] *= alpha[qc];
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) acc[qc][nb] *= alpha[qc];
+      }
+    }
+#pragma unroll
+    for (int qc = 0; qc < QC; ++qc) {
+      const float ms = m[qc] == kNegInf ? 0.0f : m[qc];  // a column with no key yet stays empty
       float ps = 0.0f;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const float pe = fast_exp2(z[e] - ms);
+        const float sc = e < 4 ? s0[qc][e] : s1[qc][e - 4];
+        const float pe = fast_exp2(__builtin_fmaf(sc, c, -ms));
         ps += pe;
         pB[qc][e] = (__bf16)pe;
       }
-      lsum[qc] = lsum[qc] * alpha[qc] + ps;
-      m[qc] = mn;
+      lsum[qc] += ps;
     }
     // V^T operand of O^T += V^T P^T: lane (c16, j4) needs channel 16nb + c16 of keys
     // 4j4..4j4+3 and 16+4j4..16+4j4+3 (the key order of P^T in the score layout).  One
@@ -237,10 +270,8 @@ void prefill_bf16_kernel(PrefillArgs a, int tq, int tiles) {
                                                             hi4[0], hi4[1], hi4[2], hi4[3]};
       const bf16x8 va = __builtin_bit_cast(bf16x8, v8);
 #pragma unroll
-      for (int qc = 0; qc < QC; ++qc) {
-        acc[qc][nb] *= alpha[qc];
+      for (int qc = 0; qc < QC; ++qc)
         acc[qc][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pB[qc], acc[qc][nb], 0, 0, 0);
-      }
     }
     __builtin_amdgcn_sched_barrier(0);
   }
