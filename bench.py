@@ -7,8 +7,9 @@ Inputs are seeded synthetic tensors already resident in HBM; rings are pre-fille
 
 Default workload (c3): batch 256, Hq 32, Hkv 8, head_dim 128, B 2048, bf16, positions
 uniform in [0, 512K).  Also reported: the same-library sliding-window ring on the same
-tensors (W = 2B = 4096 in 4096 slots, plus the paper-matched W = B), and the ragged GQA-8
-workload (c4).
+tensors (W = 2B = 4096 in 4096 slots, plus the paper-matched W = B), the ragged GQA-8
+workload (c4), the paper-shape latency sweep, and prefill (PBB and SWA) in TFLOP/s against
+the bf16 matrix-core peak.
 
 Prints ONE JSON line.  Roofline: algorithmic bytes of the support actually read (ring K and
 V rows of |A(t)| - 1 sources, q, out, the new K/V and their slot write, pos) divided by the
@@ -48,8 +49,9 @@ def step_bytes(t, cfg):
 
 
 def _kernel_hash():
+    """Hash of the sources that define the decode kernels (counter summaries are tied to it)."""
     h = hashlib.sha256()
-    for f in ("pbb_kernels.hip", "pbb_api.cpp", "pbb_internal.h"):
+    for f in ("pbb_kernels.hip", "pbb_device.h"):
         with open(os.path.join(ROOT, "paper_2606_02680_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -137,6 +139,75 @@ class Workload:
         elapsed = time.perf_counter() - w0
         kern = sum(s.elapsed_time(e) for s, e in zip(starts, ends)) / 1e3 / steps
         return elapsed, kern, total_bytes
+
+
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+
+# Prefill workloads (prompts at positions 0..n-1): c3's head shapes with a 16K prompt, and the
+# paper's model shape (Hq 12, Hkv 2, d 64, B 128) with a 64K prompt.
+PREFILL_SHAPES = (
+    ("prefill_c3_shapes_pbb_b2048_n16384", dict(batch=4, n=16384, hq=32, hkv=8, d=128, block=2048)),
+    ("prefill_c3_shapes_swa_w4096_n16384", dict(batch=4, n=16384, hq=32, hkv=8, d=128, window=4096)),
+    ("prefill_paper_shape_pbb_b128_n65536", dict(batch=1, n=65536, hq=12, hkv=2, d=64, block=128)),
+    ("prefill_paper_shape_swa_w128_n65536", dict(batch=1, n=65536, hq=12, hkv=2, d=64, window=128)),
+)
+
+
+def prefill_support_total(n, block=0, window=0):
+    """sum over t < n of |A(t)| (PBB interval form, or the window)."""
+    import torch
+    t = torch.arange(n, dtype=torch.int64)
+    if block:
+        h = block // 2
+        lo = torch.clamp(h * (torch.div(t, h, rounding_mode="floor") - 1), min=0)
+    else:
+        lo = torch.clamp(t - window + 1, min=0)
+    return int((t - lo + 1).sum())
+
+
+def prefill_measure(device, batch, n, hq, hkv, d, block=0, window=0, reps=10):
+    """Median kernel time of one prefill launch (HIP events on the launch stream) and its
+    algorithmic rate: 4 * d * Hq * batch * sum_t |A(t)| FLOP (scores and value products)."""
+    import torch
+    import paper_2606_02680_amd as P
+    import workloads as W
+    mode = "pbb" if block else "swa"
+    cfg = W.Config(f"prefill-{mode}", mode, batch=batch, hq=hq, hkv=hkv, d=d, block=block,
+                   slots=block or window, window=window, dtype="bf16", seed=7, value_scale=1.0,
+                   pos_hi=0, steps=1)
+    q, k, v = W.prompt(cfg, n, device=device)
+    if block:
+        desc = P.make_desc(batch, hq, hkv, d, block=block, dtype=torch.bfloat16)
+        fn = P.pbb_prefill
+    else:
+        desc = P.make_desc(batch, hq, hkv, d, window=window, slots=window, dtype=torch.bfloat16)
+        fn = P.swa_prefill
+    out = torch.empty_like(q)
+    lse = torch.empty((batch, hq, n), dtype=torch.float32, device=device)
+    kr, vr = P.alloc_rings(desc, device)
+    stream = torch.cuda.current_stream()
+    for _ in range(2):
+        fn(desc, q, k, v, out, lse, kr, vr, stream=stream)
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(reps)]
+    for e0, e1 in ev:
+        e0.record(stream)
+        fn(desc, q, k, v, out, lse, kr, vr, stream=stream)
+        e1.record(stream)
+    torch.cuda.synchronize()
+    ms = sorted(e0.elapsed_time(e1) for e0, e1 in ev)[reps // 2]
+    flops = 4.0 * d * hq * batch * prefill_support_total(n, block, window)
+    tflops = flops / (ms * 1e-3) / 1e12
+    return {"kernel_ms": ms, "tflops": tflops, "frac_of_bf16_mfma_peak": tflops / MFMA_BF16_PEAK_TFLOPS,
+            "tokens_per_s": batch * n / (ms * 1e-3), "algorithmic_tflop": flops / 1e12}
+
+
+def prefill_extras(device):
+    res = {}
+    for name, shape in PREFILL_SHAPES:
+        res[name] = prefill_measure(device, **shape)
+    return res
 
 
 PAPER_ORIGINS = (8192, 16384, 32768, 65536, 131072, 262144, 524288, 1048576)
@@ -255,6 +326,8 @@ def main(argv=None):
                     help="skip the SWA-ring and ragged-batch comparison runs")
     ap.add_argument("--paper-latency", action="store_true",
                     help="only run the paper-shape latency sweep (3 shapes x 8 origins)")
+    ap.add_argument("--prefill", action="store_true",
+                    help="only run the prefill measurements (c3 head shapes and paper shape)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only time a plain 1 GiB device copy (HBM counter calibration)")
     args = ap.parse_args(argv)
@@ -285,6 +358,10 @@ def main(argv=None):
         el = (time.perf_counter() - w0) / 5
         print(json.dumps({"copy_probe_bytes_read": 2 * n, "copy_probe_bytes_written": 2 * n,
                           "copy_probe_gbps_read_plus_write": 4 * n / el / 1e9}), flush=True)
+        return 0
+
+    if args.prefill:
+        print(json.dumps({"prefill": prefill_extras(device)}), flush=True)
         return 0
 
     if args.paper_latency:
@@ -362,6 +439,7 @@ def main(argv=None):
         torch.cuda.empty_cache()
         extra["paper_shape_latency_us_per_step"] = paper_latency(
             device, shapes=(10, 12, 14), origins=(8192, 1048576))
+        extra["prefill"] = prefill_extras(device)
         result["extra"] = extra
         result["paper_context"] = ("Flash-PBB 1.82x Flash-SWA decode-core throughput on an RTX "
                                    "4090 (48 GB), BF16, batch 1, Hkv 2, d 64, b 128 vs w 128")
