@@ -41,6 +41,16 @@ __device__ __forceinline__ int support_lo(const PrefillArgs& a, int t) {
   return lo > 0 ? lo : 0;
 }
 
+// Transposed LDS read (gfx950 ds_read_b64_tr_b16) at addr + OFF.  Issued as inline asm: the
+// compiler cannot tell these reads apart from the LDS DMA still in flight and would otherwise
+// wait for every outstanding load before each of them.  The caller waits with lds_wait_regs.
+template <int OFF>
+__device__ __forceinline__ u32x2 tr_read(uint32_t addr) {
+  u32x2 r;
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(OFF));
+  return r;
+}
+
 template <int D, int QC>
 __global__ __launch_bounds__(kPrefillWaves * 64) __attribute__((amdgpu_waves_per_eu(2)))
 void prefill_bf16_kernel(PrefillArgs a, int tq, int tiles) {
@@ -119,6 +129,16 @@ void prefill_bf16_kernel(PrefillArgs a, int tq, int tiles) {
   // V rows are stored whole, 32-byte chunk c of row r at chunk c ^ (r mod 4), so that the
   // transposed reads below (4 rows x 32 bytes per 16 lanes) spread over all banks.
   auto swz_v = [](int r) -> int { return 2 * (r & 3); };  // in 16-byte pieces
+  // LDS byte addresses of this lane's transposed V reads in stage 0, for chunks nb = 0..3
+  // (chunks 4..7 of d = 128 rows sit 128 bytes further: (nb ^ q) = 4 + ((nb - 4) ^ q)).
+  uint32_t vaddr[4];
+  {
+    const uint32_t base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) unsigned char*)smem;
+    const int vrow = 4 * j4 + (c16 >> 2);
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      vaddr[q] = base + KTILE + vrow * ROWB + ((((q ^ (c16 >> 2)) << 5) | ((c16 & 3) << 3)));
+  }
 
   // This wave's share of the DMA of a step: MYOPS 1 KiB pieces, each lane one 16-byte piece of
   // one key row.  Row pointers start at the first step and advance 32 rows per step; in the
@@ -255,20 +275,41 @@ void prefill_bf16_kernel(PrefillArgs a, int tq, int tiles) {
     // 4j4..4j4+3 and 16+4j4..16+4j4+3 (the key order of P^T in the score layout).  One
     // transposed read per half: within each 16-lane group, lane i names 4 channels
     // 16nb + 4(i mod 4) .. +3 of key row 4j4 + i/4, and lane c16 receives channel 16nb + c16 of
-    // those four rows.
-    const unsigned char* vt = tile_p + KTILE;
-    const int vrow = 4 * j4 + (c16 >> 2);
+    // those four rows.  Chunk nb of that row sits at nb ^ (row mod 4) = nb ^ (c16 / 4).
+    const uint32_t sb = (uint32_t)((st % STAGES) * BUF);
+    u32x2 vr[2 * NB];
+    constexpr int HI = 16 * ROWB;   // rows 16.. of the tile
+    vr[0] = tr_read<0>(vaddr[0] + sb);
+    vr[1] = tr_read<HI>(vaddr[0] + sb);
+    vr[2] = tr_read<0>(vaddr[1] + sb);
+    vr[3] = tr_read<HI>(vaddr[1] + sb);
+    vr[4] = tr_read<0>(vaddr[2] + sb);
+    vr[5] = tr_read<HI>(vaddr[2] + sb);
+    vr[6] = tr_read<0>(vaddr[3] + sb);
+    vr[7] = tr_read<HI>(vaddr[3] + sb);
+    if constexpr (NB == 8) {
+      vr[8] = tr_read<128>(vaddr[0] + sb);
+      vr[9] = tr_read<HI + 128>(vaddr[0] + sb);
+      vr[10] = tr_read<128>(vaddr[1] + sb);
+      vr[11] = tr_read<HI + 128>(vaddr[1] + sb);
+      vr[12] = tr_read<128>(vaddr[2] + sb);
+      vr[13] = tr_read<HI + 128>(vaddr[2] + sb);
+      vr[14] = tr_read<128>(vaddr[3] + sb);
+      vr[15] = tr_read<HI + 128>(vaddr[3] + sb);
+      asm volatile("s_waitcnt lgkmcnt(0)"
+                   : "+v"(vr[0]), "+v"(vr[1]), "+v"(vr[2]), "+v"(vr[3]), "+v"(vr[4]),
+                     "+v"(vr[5]), "+v"(vr[6]), "+v"(vr[7]), "+v"(vr[8]), "+v"(vr[9]),
+                     "+v"(vr[10]), "+v"(vr[11]), "+v"(vr[12]), "+v"(vr[13]), "+v"(vr[14]),
+                     "+v"(vr[15]));
+    } else {
+      asm volatile("s_waitcnt lgkmcnt(0)"
+                   : "+v"(vr[0]), "+v"(vr[1]), "+v"(vr[2]), "+v"(vr[3]), "+v"(vr[4]),
+                     "+v"(vr[5]), "+v"(vr[6]), "+v"(vr[7]));
+    }
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
-      const int off = (((nb ^ (c16 >> 2)) << 5) | ((c16 & 3) << 3));
-      typedef __attribute__((ext_vector_type(4))) short i16x4;
-      const i16x4 lo4 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-          (__attribute__((address_space(3))) i16x4*)(vt + vrow * ROWB + off));
-      const i16x4 hi4 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-          (__attribute__((address_space(3))) i16x4*)(vt + (vrow + 16) * ROWB + off));
-      const __attribute__((ext_vector_type(8))) short v8 = {lo4[0], lo4[1], lo4[2], lo4[3],
-                                                            hi4[0], hi4[1], hi4[2], hi4[3]};
-      const bf16x8 va = __builtin_bit_cast(bf16x8, v8);
+      const u32x4 w = {vr[2 * nb][0], vr[2 * nb][1], vr[2 * nb + 1][0], vr[2 * nb + 1][1]};
+      const bf16x8 va = __builtin_bit_cast(bf16x8, w);
 #pragma unroll
       for (int qc = 0; qc < QC; ++qc)
         acc[qc][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pB[qc], acc[qc][nb], 0, 0, 0);
