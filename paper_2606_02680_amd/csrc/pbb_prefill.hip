@@ -21,6 +21,8 @@
 // copies those of its positions that fall in the last `slots` positions of the prompt into the
 // ring (slot s mod slots, Appendix F.1), the state decode continues from.
 
+#include <type_traits>
+
 #include "pbb_device.h"
 #include "pbb_internal.h"
 
@@ -39,6 +41,23 @@ __device__ __forceinline__ int support_lo(const PrefillArgs& a, int t) {
   }
   const int lo = t - a.window + 1;
   return lo > 0 ? lo : 0;
+}
+
+// Value of lane l ^ 16 and of lane l ^ 32 (gfx950 v_permlane16_swap / v_permlane32_swap with
+// both operands x: one result is the lane's own value, the other its partner's), on the VALU
+// instead of an LDS permute.
+__device__ __forceinline__ float max_xor16_32(float x) {
+  auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+
+__device__ __forceinline__ float sum_xor16_32(float x) {
+  auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
 // Transposed LDS read (gfx950 ds_read_b64_tr_b16) at addr + OFF.  Issued as inline asm: the
@@ -188,7 +207,7 @@ void prefill_bf16_kernel(PrefillArgs a, int tq, int tiles) {
   issue(0, 0);
   if (nsteps > 1) issue(1, 1);
 
-  for (int st = 0; st < nsteps; ++st) {
+  auto step = [&](int st, auto masked) {
     // This wave's loads of step st have landed once at most step st+1's are outstanding; the
     // barrier then covers every wave's loads, and every wave is done with step st-1, whose
     // stage the loads of step st+2 reuse.
@@ -202,7 +221,6 @@ void prefill_bf16_kernel(PrefillArgs a, int tq, int tiles) {
 
     const unsigned char* tile_p = smem + (st % STAGES) * BUF;
     const int k0 = (s_first + st) * 32;
-    const bool interior = k0 >= mask_lo && k0 + 31 <= mask_hi;
     f32x4 s0[QC], s1[QC];
 #pragma unroll
     for (int qc = 0; qc < QC; ++qc) {
@@ -235,15 +253,14 @@ void prefill_bf16_kernel(PrefillArgs a, int tq, int tiles) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         float sc = e < 4 ? s0[qc][e] : s1[qc][e - 4];
-        if (!interior) {
+        if constexpr (decltype(masked)::value) {
           const int key = k0 + (e < 4 ? 4 * j4 + e : 16 + 4 * j4 + (e - 4));
           sc = (key >= lo_c[qc] && key <= hi_c[qc]) ? sc : kNegInf;
           if (e < 4) s0[qc][e] = sc; else s1[qc][e - 4] = sc;
         }
         mx = fmaxf(mx, sc);
       }
-      mx = fmaxf(mx, __shfl_xor(mx, 16));
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      mx = max_xor16_32(mx);
       const float cand = mx * c;
       const bool grow = cand > m[qc] + 8.0f;
       alpha[qc] = grow ? fast_exp2(m[qc] - cand) : 1.0f;
@@ -315,14 +332,23 @@ void prefill_bf16_kernel(PrefillArgs a, int tq, int tiles) {
         acc[qc][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pB[qc], acc[qc][nb], 0, 0, 0);
     }
     __builtin_amdgcn_sched_barrier(0);
-  }
+  };
+
+  // Steps whose 32 keys all lie in every position's support need no mask: they form one run
+  // [st_a, st_b); the steps before (a ragged interval start) and after (the causal diagonal)
+  // are masked.
+  int st_a = (mask_lo + 31) / 32 - s_first;
+  int st_b = (mask_hi + 1) / 32 - s_first;
+  st_a = max(0, min(st_a, nsteps));
+  st_b = max(st_a, min(st_b, nsteps));
+  for (int st = 0; st < st_a; ++st) step(st, std::true_type{});
+  for (int st = st_a; st < st_b; ++st) step(st, std::false_type{});
+  for (int st = st_b; st < nsteps; ++st) step(st, std::true_type{});
 
   // Outputs: o = acc / l (bf16 RNE), lse = (m + log2 l) * ln 2.
 #pragma unroll
   for (int qc = 0; qc < QC; ++qc) {
-    float l = lsum[qc];
-    l += __shfl_xor(l, 16);
-    l += __shfl_xor(l, 32);
+    const float l = sum_xor16_32(lsum[qc]);
     if (!valid[qc]) continue;
     const float inv = 1.0f / l;
     uint16_t* orow = (uint16_t*)a.out + ((size_t)(b * (size_t)n + tcol[qc]) * a.hq + hcol[qc]) * D;
