@@ -15,6 +15,8 @@ Layers?"):
 * Sec. 3, Eq.(attention) -- one softmax over the support with scores ``q.k / sqrt(d_h)``.
 * Appendix F.1, Proposition "Relocation-free PBB cache" -- position ``s`` is stored at slot
   ``s mod b``; :func:`expected_ring` gives the ring image that sequential appends produce.
+* Appendix C -- rotary positions with base 10^6 (RoPE); half-split channel pairs as in the
+  Qwen2.5 decoders the paper trains (:func:`rope`, ``decode(..., rope_base=...)``).
 * Appendix A.4, Eq.(lse) -- the log-partition ``log sum_s e^{z_s}`` that :func:`prefill` also
   returns for every prompt position (the quantity a tiled prefill rescales with).
 
@@ -75,6 +77,11 @@ def _load():
     lib.oracle_decode.argtypes = [i32, i64, i64, i64, i64, i64, i64, vp, vp, vp, vp, vp, i64,
                                   dbl, vp, i32]
     lib.oracle_decode.restype = i32
+    lib.oracle_rope.argtypes = [i64, i64, dbl, vp, vp]
+    lib.oracle_rope.restype = None
+    lib.oracle_decode_rope.argtypes = [i32, i64, i64, i64, i64, i64, i64, vp, vp, vp, vp, vp,
+                                       i64, dbl, dbl, vp, i32]
+    lib.oracle_decode_rope.restype = i32
     lib.oracle_prefill.argtypes = [i32, i64, i64, i64, i64, i64, i64, i64, vp, vp, vp, dbl, vp,
                                    vp, i32]
     lib.oracle_prefill.restype = i32
@@ -150,14 +157,27 @@ def attend(q: np.ndarray, k: np.ndarray, v: np.ndarray, scale: float | None = No
     return o, lse.value
 
 
+def rope(x, pos: int, base: float) -> np.ndarray:
+    """Rotary position embedding of head vector(s) ``x`` [..., d] at absolute position ``pos``
+    (half-split pairs c, c + d/2; angle ``pos * base^(-2c/d)``), fp64."""
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    d = x.shape[-1]
+    flat = x.reshape(-1, d)
+    out = np.empty_like(flat)
+    for r in range(flat.shape[0]):
+        _load().oracle_rope(d, int(pos), float(base), _ptr(flat[r]), _ptr(out[r]))
+    return out.reshape(x.shape)
+
+
 def decode(mode: int, pos, q, k_hist, v_hist, hist_lo, *, block: int = 0, window: int = 0,
-           scale: float | None = None, n_threads: int = 0) -> np.ndarray:
+           scale: float | None = None, n_threads: int = 0, rope_base: float = 0.0) -> np.ndarray:
     """One batched decode step in fp64.
 
     ``pos``: int [batch] absolute positions t.  ``q``: [batch][Hq][d].
     ``k_hist``/``v_hist``: [batch][Hkv][hist_len][d] with absolute position ``s`` of sequence
     ``b`` stored at row ``s - hist_lo[b]``.  ``mode`` is :data:`PBB` (support Eq.(pbb) with
-    ``h = block/2``) or :data:`SWA` (support of Prop. 2 with ``window``).
+    ``h = block/2``) or :data:`SWA` (support of Prop. 2 with ``window``).  ``rope_base > 0``
+    rotates q at ``pos`` and each (unrotated) history key at its own position (:func:`rope`).
     Returns float64 [batch][Hq][d].
     """
     pos = np.ascontiguousarray(pos, dtype=np.int64)
@@ -173,9 +193,15 @@ def decode(mode: int, pos, q, k_hist, v_hist, hist_lo, *, block: int = 0, window
     if scale is None:
         scale = 1.0 / np.sqrt(d)
     out = np.zeros((batch, hq, d), dtype=np.float64)
-    rc = _load().oracle_decode(int(mode), batch, hq, hkv, d, int(block), int(window), _ptr(pos),
-                               _ptr(q), _ptr(k_hist), _ptr(v_hist), _ptr(hist_lo), hist_len,
-                               float(scale), _ptr(out), int(n_threads))
+    if rope_base:
+        rc = _load().oracle_decode_rope(int(mode), batch, hq, hkv, d, int(block), int(window),
+                                        _ptr(pos), _ptr(q), _ptr(k_hist), _ptr(v_hist),
+                                        _ptr(hist_lo), hist_len, float(scale), float(rope_base),
+                                        _ptr(out), int(n_threads))
+    else:
+        rc = _load().oracle_decode(int(mode), batch, hq, hkv, d, int(block), int(window),
+                                   _ptr(pos), _ptr(q), _ptr(k_hist), _ptr(v_hist), _ptr(hist_lo),
+                                   hist_len, float(scale), _ptr(out), int(n_threads))
     if rc == 1:
         raise ValueError("oracle.decode: a support position is missing from the history")
     if rc != 0:

@@ -12,6 +12,7 @@
  *       A(t) = {p..t}  union  {p-h..p-1} if p > 0 and 0 <= r < h, else nothing
  *   - the sliding-window support {max(0,t-w+1)..t}                         Prop. 2 (Sec. 2.2)
  *   - single-softmax attention over a support, scores q.k/sqrt(d)          Sec. 3, Eq.(attention)
+ *   - rotary positions (RoPE, base 10^6 in the paper's models), half-split pairs  Appendix C
  *   - prefill: every prompt position over its own support, with its log-partition
  *     log sum_s e^{z_s}                                                    Appendix A.4, Eq.(lse)
  * Keys and values are read from HISTORY arrays indexed by absolute position, never from
@@ -114,6 +115,26 @@ void oracle_attend(int64_t n, int64_t d, const double *q, const double *k, const
     free(z);
 }
 
+/*
+ * Rotary position embedding of one head vector at absolute position `pos` (the models of the
+ * paper use RoPE with base 10^6, Appendix C).  Half-split pairing, as in the Qwen2.5 decoders
+ * the paper trains: channel c < d/2 pairs with c + d/2 and turns by the angle
+ * pos * base^(-2c/d):
+ *   out[c]       = x[c] cos(a) - x[c + d/2] sin(a)
+ *   out[c + d/2] = x[c + d/2] cos(a) + x[c] sin(a)
+ * Everything in fp64 (the angle itself is exact to ~1e-16 relative).
+ */
+void oracle_rope(int64_t d, int64_t pos, double base, const double *x, double *out) {
+    const int64_t half = d / 2;
+    for (int64_t c = 0; c < half; ++c) {
+        const double ang = (double)pos * pow(base, -2.0 * (double)c / (double)d);
+        const double cs = cos(ang), sn = sin(ang);
+        const double a = x[c], b = x[c + half];
+        out[c] = a * cs - b * sn;
+        out[c + half] = b * cs + a * sn;
+    }
+}
+
 /* ------------------------------------------------------------------------------------ */
 /* Batched decode over absolute-position history.                                        */
 
@@ -127,6 +148,7 @@ typedef struct {
     const int64_t *hist_lo;
     int64_t hist_len;
     double scale;
+    double rope_base; /* > 0: rotate q at t and every key at its own position (oracle_rope) */
     double *out; /* [batch][Hq][d] */
     int64_t next;       /* next (b, head) work item */
     int error;
@@ -148,6 +170,12 @@ static void decode_one(decode_job *j, int64_t item, double *z, double *qd) {
     for (int64_t c = 0; c < d; ++c) o[c] = 0.0;
     if (t < 0) return;
     for (int64_t c = 0; c < d; ++c) qd[c] = (double)j->q[(b * j->n_q_heads + i) * d + c];
+    double *kr = qd + d; /* scratch: one rotated key row, then the raw row */
+    double *kraw = qd + 2 * d;
+    if (j->rope_base > 0.0) {
+        for (int64_t c = 0; c < d; ++c) kraw[c] = qd[c];
+        oracle_rope(d, t, j->rope_base, kraw, qd);
+    }
     /* Candidate window: wide enough to contain every source either definition admits. */
     int64_t span = (j->mode == 0) ? (j->block + j->block / 2) : j->window;
     int64_t lo = t - span;
@@ -164,7 +192,13 @@ static void decode_one(decode_job *j, int64_t item, double *z, double *qd) {
             return;
         }
         double acc = 0.0;
-        for (int64_t c = 0; c < d; ++c) acc += qd[c] * (double)kh[row * d + c];
+        if (j->rope_base > 0.0) {
+            for (int64_t c = 0; c < d; ++c) kraw[c] = (double)kh[row * d + c];
+            oracle_rope(d, s, j->rope_base, kraw, kr);
+            for (int64_t c = 0; c < d; ++c) acc += qd[c] * kr[c];
+        } else {
+            for (int64_t c = 0; c < d; ++c) acc += qd[c] * (double)kh[row * d + c];
+        }
         z[s - lo] = acc * j->scale;
         if (z[s - lo] > m) m = z[s - lo];
         ++cnt;
@@ -185,7 +219,7 @@ static void *decode_worker(void *arg) {
     decode_job *j = (decode_job *)arg;
     int64_t span = (j->mode == 0) ? (j->block + j->block / 2) : j->window;
     double *z = (double *)malloc(sizeof(double) * (size_t)(span + 1));
-    double *qd = (double *)malloc(sizeof(double) * (size_t)j->head_dim);
+    double *qd = (double *)malloc(sizeof(double) * (size_t)(3 * j->head_dim));
     const int64_t total = j->batch * j->n_q_heads;
     for (;;) {
         pthread_mutex_lock(&j->lock);
@@ -207,11 +241,41 @@ static void *decode_worker(void *arg) {
  * position lies outside [hist_lo[b], hist_lo[b] + hist_len), 2 on bad arguments.
  * n_threads <= 0 uses every online core.
  */
+static int decode_run(int mode, int64_t batch, int64_t n_q_heads, int64_t n_kv_heads,
+                      int64_t head_dim, int64_t block, int64_t window, const int64_t *pos,
+                      const float *q, const float *k_hist, const float *v_hist,
+                      const int64_t *hist_lo, int64_t hist_len, double scale, double rope_base,
+                      double *out, int n_threads);
+
 int oracle_decode(int mode, int64_t batch, int64_t n_q_heads, int64_t n_kv_heads,
                   int64_t head_dim, int64_t block, int64_t window, const int64_t *pos,
                   const float *q, const float *k_hist, const float *v_hist,
                   const int64_t *hist_lo, int64_t hist_len, double scale, double *out,
                   int n_threads) {
+    return decode_run(mode, batch, n_q_heads, n_kv_heads, head_dim, block, window, pos, q,
+                      k_hist, v_hist, hist_lo, hist_len, scale, 0.0, out, n_threads);
+}
+
+/*
+ * oracle_decode with rotary positions: q at its position t and every history key at its own
+ * absolute position s are rotated by oracle_rope (base rope_base > 0) before the scores; the
+ * history holds unrotated keys, values are not rotated.
+ */
+int oracle_decode_rope(int mode, int64_t batch, int64_t n_q_heads, int64_t n_kv_heads,
+                       int64_t head_dim, int64_t block, int64_t window, const int64_t *pos,
+                       const float *q, const float *k_hist, const float *v_hist,
+                       const int64_t *hist_lo, int64_t hist_len, double scale, double rope_base,
+                       double *out, int n_threads) {
+    if (!(rope_base > 1.0) || head_dim % 2 != 0) return 2;
+    return decode_run(mode, batch, n_q_heads, n_kv_heads, head_dim, block, window, pos, q,
+                      k_hist, v_hist, hist_lo, hist_len, scale, rope_base, out, n_threads);
+}
+
+static int decode_run(int mode, int64_t batch, int64_t n_q_heads, int64_t n_kv_heads,
+                      int64_t head_dim, int64_t block, int64_t window, const int64_t *pos,
+                      const float *q, const float *k_hist, const float *v_hist,
+                      const int64_t *hist_lo, int64_t hist_len, double scale, double rope_base,
+                      double *out, int n_threads) {
     if (batch < 0 || n_q_heads <= 0 || n_kv_heads <= 0 || head_dim <= 0) return 2;
     if (n_q_heads % n_kv_heads != 0) return 2;
     if (mode == 0 && (block < 2 || block % 2 != 0)) return 2;
@@ -232,6 +296,7 @@ int oracle_decode(int mode, int64_t batch, int64_t n_q_heads, int64_t n_kv_heads
     j.hist_lo = hist_lo;
     j.hist_len = hist_len;
     j.scale = scale;
+    j.rope_base = rope_base;
     j.out = out;
     pthread_mutex_init(&j.lock, NULL);
     if (n_threads <= 0) n_threads = (int)sysconf(_SC_NPROCESSORS_ONLN);

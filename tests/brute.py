@@ -23,6 +23,21 @@ def coverage_mask(n: int, block: int, bridge: int | None = None) -> np.ndarray:
     return np.where(initial, causal, cov)
 
 
+def coverage_mask_window(t_lo: int, nt: int, s_lo: int, ns: int, block: int,
+                         bridge: int | None = None) -> np.ndarray:
+    """Bool [nt][ns]: the coverage mask of targets t_lo .. t_lo+nt-1 over sources
+    s_lo .. s_lo+ns-1 (same rule as :func:`coverage_mask`, on absolute positions)."""
+    h = block // 2 if bridge is None else bridge
+    t = t_lo + np.arange(nt).reshape(-1, 1)
+    s = s_lo + np.arange(ns).reshape(1, -1)
+    dist = t - s
+    r = t % block
+    initial = (t // block) == 0
+    cov = ((dist >= 0) & (dist <= r)) | ((r < h) & (dist > r) & (dist <= r + h))
+    causal = dist >= 0
+    return np.where(initial, causal, cov)
+
+
 def interval_start(t: int, block: int) -> int:
     """Left end a(t) = max(0, h*(floor(t/h) - 1)) of the interval form (Sec. 3 "Flash-PBB";
     Appendix A.3, Eq.(pbb_relay)), h = block/2."""

@@ -132,3 +132,10 @@ def test_kv_bytes(golden):
     """Local KV storage 2 * batch * b * H_KV * d_h * u (Appendix F.1)."""
     batch, b, hkv, d, u = 1, 128, 2, 64, 2
     assert 2 * batch * b * hkv * d * u == golden["local_kv_bytes_batch1_b128_hkv2_d64_bf16"]
+
+
+def test_windowed_coverage_mask_matches_full_mask():
+    from tests.brute import coverage_mask_window
+    full = coverage_mask(300, 16)
+    np.testing.assert_array_equal(coverage_mask_window(100, 50, 60, 90, 16), full[100:150, 60:150])
+    np.testing.assert_array_equal(coverage_mask_window(0, 40, 0, 40, 16), full[:40, :40])
