@@ -22,8 +22,8 @@ MUTATIONS = {
     "bridge_start_off_by_one": ("s >= p - bridge && s <= p - 1", "s > p - bridge && s <= p - 1"),
     "block_start_dropped": ("if (s >= p) return 1;", "if (s > p) return 1;"),
     "bridge_wrong_half": ("s >= p - bridge && s <= p - 1", "s >= p - 2 * bridge && s <= p - bridge - 1"),
-    "scale_dropped": ("(double)kh[row * d + c];\n        z[s - lo] = acc * j->scale;",
-                      "(double)kh[row * d + c];\n        z[s - lo] = acc;"),
+    "scale_dropped": ("(double)kh[row * d + c];\n        }\n        z[s - lo] = acc * j->scale;",
+                      "(double)kh[row * d + c];\n        }\n        z[s - lo] = acc;"),
     "exp_sign_flipped": ("int64_t row = s - j->hist_lo[b];\n        double w = exp(z[s - lo] - m);",
                          "int64_t row = s - j->hist_lo[b];\n        double w = exp(m - z[s - lo]);"),
     "gqa_strided": ("const int64_t g = i / G; /* query head i reads KV head floor(i/G) */\n    const int64_t t = j->pos[b];",
