@@ -68,6 +68,14 @@ typedef enum {
  *   PBB: block even, 2 <= block <= 65536, slots == block (the ring has exactly B slots);
  *   SWA: 1 <= window <= slots <= 65536 (block is ignored).
  * scale <= 0 selects 1/sqrt(head_dim) (Sec. 3, Eq.(attention)).
+ * rope_base > 1 (bfloat16 decode only; PBB_ERR_DTYPE for float32): the decode step applies the
+ * rotary position embedding itself (the paper's models use RoPE with base 10^6, Appendix C):
+ * q and k_new are turned by their absolute position t before the scores, channel c < d/2
+ * pairing with c + d/2 at angle t * rope_base^(-2c/d) (half-split pairs, as in the Qwen2.5
+ * decoders the paper trains), rounded to bf16, and the turned key is what the ring receives,
+ * so the ring holds rotated keys (slot mapping unchanged: positions stay absolute, Appendix
+ * F.1).  v is not rotated.  Prefill takes already-rotated inputs and requires rope_base == 0.
+ * rope_base == 0 leaves q and k_new as given; other values give PBB_ERR_SHAPE.
  */
 typedef struct {
   int32_t batch;
@@ -79,6 +87,7 @@ typedef struct {
   int32_t slots;   /* ring slots per (sequence, KV head) */
   int32_t dtype;   /* a pbb_dtype_t */
   float scale;
+  float rope_base; /* 0: no rotary embedding; > 1: see below */
 } pbb_desc_t;
 
 /* Human-readable name of a status code (static storage; never NULL). */
@@ -176,7 +185,8 @@ pbb_status_t swa_decode_step_advance(const pbb_desc_t *desc, const int32_t *pos,
  *            pbb_ring_init and this call, decoding continues with pos[b] = n (Appendix F.1).
  * bfloat16 only (PBB_ERR_DTYPE otherwise); fp32 accumulation, output rounded RNE.  Requires
  * 0 <= n <= 2^30; n == 0 does nothing.  q, k, v, out, rings 16-byte aligned, lse 4-byte
- * aligned.  Same descriptor rules as pbb_decode_step; no workspace.
+ * aligned.  Same descriptor rules as pbb_decode_step, and rope_base must be 0 (rotate q and k
+ * before the call; the ring then holds rotated keys as a rotary decode expects); no workspace.
  */
 pbb_status_t pbb_prefill(const pbb_desc_t *desc, int32_t n, const void *q, const void *k,
                          const void *v, void *out, float *lse, void *k_ring, void *v_ring,

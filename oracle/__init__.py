@@ -79,6 +79,8 @@ def _load():
     lib.oracle_decode.restype = i32
     lib.oracle_rope.argtypes = [i64, i64, dbl, vp, vp]
     lib.oracle_rope.restype = None
+    lib.oracle_rope_rows.argtypes = [i64, i64, vp, dbl, vp, vp]
+    lib.oracle_rope_rows.restype = None
     lib.oracle_decode_rope.argtypes = [i32, i64, i64, i64, i64, i64, i64, vp, vp, vp, vp, vp,
                                        i64, dbl, dbl, vp, i32]
     lib.oracle_decode_rope.restype = i32
@@ -166,6 +168,18 @@ def rope(x, pos: int, base: float) -> np.ndarray:
     out = np.empty_like(flat)
     for r in range(flat.shape[0]):
         _load().oracle_rope(d, int(pos), float(base), _ptr(flat[r]), _ptr(out[r]))
+    return out.reshape(x.shape)
+
+
+def rope_rows(x, pos, base: float) -> np.ndarray:
+    """:func:`rope` of every row of ``x`` [..., L, d] (float32 values) at its position ``pos``
+    (int, broadcastable to ``x.shape[:-1]``); fp64 result of ``x``'s shape."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    d = x.shape[-1]
+    p = np.ascontiguousarray(np.broadcast_to(np.asarray(pos, dtype=np.int64), x.shape[:-1]))
+    flat = x.reshape(-1, d)
+    out = np.empty(flat.shape, dtype=np.float64)
+    _load().oracle_rope_rows(d, flat.shape[0], _ptr(p), float(base), _ptr(flat), _ptr(out))
     return out.reshape(x.shape)
 
 

@@ -124,15 +124,40 @@ void oracle_attend(int64_t n, int64_t d, const double *q, const double *k, const
  *   out[c + d/2] = x[c + d/2] cos(a) + x[c] sin(a)
  * Everything in fp64 (the angle itself is exact to ~1e-16 relative).
  */
-void oracle_rope(int64_t d, int64_t pos, double base, const double *x, double *out) {
+static void rope_freqs(int64_t d, double base, double *freq) {
+    for (int64_t c = 0; c < d / 2; ++c) freq[c] = pow(base, -2.0 * (double)c / (double)d);
+}
+
+static void rope_apply(int64_t d, int64_t pos, const double *freq, const double *x, double *out) {
     const int64_t half = d / 2;
     for (int64_t c = 0; c < half; ++c) {
-        const double ang = (double)pos * pow(base, -2.0 * (double)c / (double)d);
+        const double ang = (double)pos * freq[c];
         const double cs = cos(ang), sn = sin(ang);
         const double a = x[c], b = x[c + half];
         out[c] = a * cs - b * sn;
         out[c + half] = b * cs + a * sn;
     }
+}
+
+void oracle_rope(int64_t d, int64_t pos, double base, const double *x, double *out) {
+    double *freq = (double *)malloc(sizeof(double) * (size_t)(d / 2 + 1));
+    rope_freqs(d, base, freq);
+    rope_apply(d, pos, freq, x, out);
+    free(freq);
+}
+
+/* oracle_rope for n rows of float32 x [n][d], row r at position pos[r]; out [n][d] fp64. */
+void oracle_rope_rows(int64_t d, int64_t n, const int64_t *pos, double base, const float *x,
+                      double *out) {
+    double *freq = (double *)malloc(sizeof(double) * (size_t)(d / 2 + 1));
+    double *row = (double *)malloc(sizeof(double) * (size_t)d);
+    rope_freqs(d, base, freq);
+    for (int64_t r = 0; r < n; ++r) {
+        for (int64_t c = 0; c < d; ++c) row[c] = (double)x[r * d + c];
+        rope_apply(d, pos[r], freq, row, out + r * d);
+    }
+    free(row);
+    free(freq);
 }
 
 /* ------------------------------------------------------------------------------------ */
@@ -149,6 +174,7 @@ typedef struct {
     int64_t hist_len;
     double scale;
     double rope_base; /* > 0: rotate q at t and every key at its own position (oracle_rope) */
+    double *rope_freq; /* base^(-2c/d), c < d/2, when rope_base > 0 */
     double *out; /* [batch][Hq][d] */
     int64_t next;       /* next (b, head) work item */
     int error;
@@ -174,7 +200,7 @@ static void decode_one(decode_job *j, int64_t item, double *z, double *qd) {
     double *kraw = qd + 2 * d;
     if (j->rope_base > 0.0) {
         for (int64_t c = 0; c < d; ++c) kraw[c] = qd[c];
-        oracle_rope(d, t, j->rope_base, kraw, qd);
+        rope_apply(d, t, j->rope_freq, kraw, qd);
     }
     /* Candidate window: wide enough to contain every source either definition admits. */
     int64_t span = (j->mode == 0) ? (j->block + j->block / 2) : j->window;
@@ -194,7 +220,7 @@ static void decode_one(decode_job *j, int64_t item, double *z, double *qd) {
         double acc = 0.0;
         if (j->rope_base > 0.0) {
             for (int64_t c = 0; c < d; ++c) kraw[c] = (double)kh[row * d + c];
-            oracle_rope(d, s, j->rope_base, kraw, kr);
+            rope_apply(d, s, j->rope_freq, kraw, kr);
             for (int64_t c = 0; c < d; ++c) acc += qd[c] * kr[c];
         } else {
             for (int64_t c = 0; c < d; ++c) acc += qd[c] * (double)kh[row * d + c];
@@ -297,6 +323,11 @@ static int decode_run(int mode, int64_t batch, int64_t n_q_heads, int64_t n_kv_h
     j.hist_len = hist_len;
     j.scale = scale;
     j.rope_base = rope_base;
+    j.rope_freq = NULL;
+    if (rope_base > 0.0) {
+        j.rope_freq = (double *)malloc(sizeof(double) * (size_t)(head_dim / 2 + 1));
+        rope_freqs(head_dim, rope_base, j.rope_freq);
+    }
     j.out = out;
     pthread_mutex_init(&j.lock, NULL);
     if (n_threads <= 0) n_threads = (int)sysconf(_SC_NPROCESSORS_ONLN);
@@ -306,6 +337,7 @@ static int decode_run(int mode, int64_t batch, int64_t n_q_heads, int64_t n_kv_h
     for (int i = 0; i < n_threads; ++i) pthread_create(&th[i], NULL, decode_worker, &j);
     for (int i = 0; i < n_threads; ++i) pthread_join(th[i], NULL);
     pthread_mutex_destroy(&j.lock);
+    free(j.rope_freq);
     return j.error ? 1 : 0;
 }
 

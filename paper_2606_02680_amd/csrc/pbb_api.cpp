@@ -35,6 +35,7 @@ pbb_status_t check_desc(const pbb_desc_t* d, bool swa) {
     if (d->block < 2 || (d->block % 2) != 0 || d->block > kMaxSlots) return PBB_ERR_SHAPE;
     if (d->slots != d->block) return PBB_ERR_SHAPE;
   }
+  if (!(d->rope_base == 0.0f || d->rope_base > 1.0f)) return PBB_ERR_SHAPE;  // NaN included
   // Ring element counts must fit comfortably in 64-bit offsets and the launch grid.
   const uint64_t rows = (uint64_t)d->batch * (uint64_t)d->n_kv_heads;
   if (rows > 0x7fffffffull) return PBB_ERR_SHAPE;
@@ -87,6 +88,18 @@ pbb_status_t decode_common(const pbb_desc_t* desc, bool swa, const int32_t* pos,
   const float scale = desc->scale > 0.0f ? desc->scale
                                          : (float)(1.0 / std::sqrt((double)desc->head_dim));
   a.scale_log2 = (float)((double)scale * 1.4426950408889634);  // log2(e)
+  a.rope = desc->rope_base > 0.0f ? 1 : 0;
+  if (a.rope) {
+    if (desc->dtype != PBB_DTYPE_BF16) return PBB_ERR_DTYPE;
+    // Turns per position of channel pair c: base^(-2c/d) / (2 pi), in double.
+    const double two_pi = 6.283185307179586476925286766559;
+    for (int c = 0; c < desc->head_dim / 2; ++c)
+      a.rope_turns[c] =
+          std::pow((double)desc->rope_base, -2.0 * (double)c / (double)desc->head_dim) / two_pi;
+    for (int c = desc->head_dim / 2; c < 64; ++c) a.rope_turns[c] = 0.0;
+  } else {
+    for (int c = 0; c < 64; ++c) a.rope_turns[c] = 0.0;
+  }
 
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   const hipError_t e = desc->dtype == PBB_DTYPE_BF16 ? pbb::launch_decode_bf16(a, desc->head_dim, s)
@@ -100,6 +113,7 @@ pbb_status_t prefill_common(const pbb_desc_t* desc, bool swa, int32_t n, const v
   const pbb_status_t st = check_desc(desc, swa);
   if (st != PBB_OK) return st;
   if (desc->dtype != PBB_DTYPE_BF16) return PBB_ERR_DTYPE;
+  if (desc->rope_base != 0.0f) return PBB_ERR_SHAPE;  // prefill takes rotated inputs
   if (n < 0 || n > kMaxPrefill) return PBB_ERR_SHAPE;
   if (!q || !k || !v || !out) return PBB_ERR_NULL;
   if ((k_ring == nullptr) != (v_ring == nullptr)) return PBB_ERR_NULL;

@@ -29,6 +29,9 @@ struct DecodeArgs {
   int32_t window;      // SWA window W
   int32_t mode;        // SupportMode
   float scale_log2;    // softmax scale times log2(e)
+  int32_t rope;        // 1: rotate q and the new key by their position (rotary embedding)
+  // Turns per position of rotary channel pair c (angle / 2 pi), c < head_dim / 2.
+  double rope_turns[64];
 };
 
 // Prefill of prompts at positions 0..n-1, validated on the host before launch.

@@ -280,7 +280,7 @@ __global__ __launch_bounds__(256) void decode_f32_kernel(DecodeArgs a) {
 // p ^ kswz(r), which spreads the 16 rows read by one MFMA operand over all banks.  V groups of
 // RPI rows are padded (and, for D = 64, the upper row quad is piece-swizzled) so that the
 // transposed reads of rows 4j+e (j = 0..3) hit 32 distinct banks.
-template <int D, int NW, bool NT>
+template <int D, int NW, bool NT, bool ROPE>
 __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
   // NT: stream the ring with the non-temporal hint (rings far larger than the caches); without
   // it, small rings that are re-read every step can stay cache-resident.
@@ -344,10 +344,33 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
   unsigned char* qtile = smem + NW * 2 * BUF + wave * QTILE;
   const int nsteps = (n_total + 31) >> 5;
 
+  // Rotary mode: queries and the new key are turned by position t inside this launch.  Their
+  // raw values and the per-channel turn rates are loaded into registers here, before any K/V
+  // load, so that the first step's vmcnt wait covers them; lanes l < PPR/2 hold the new key's
+  // pieces l and l + PPR/2 (channels 8l.. and d/2 + 8l..), which pair up under the rotation.
+  u32x4 qraw[ROPE ? KK : 1];
+  u32x4 krot_lo = {0u, 0u, 0u, 0u}, krot_hi = {0u, 0u, 0u, 0u};
+  double qturn[ROPE ? 4 * KK : 1], kturn[8];
+  if constexpr (ROPE) {
+    const uint16_t* qrow = (const uint16_t*)a.q + ((size_t)b * a.hq + (size_t)g * G +
+                                                   (size_t)(c16 < G ? c16 : G - 1)) * D;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) qraw[kk] = *(const u32x4*)(qrow + 32 * kk + 8 * j4);
+#pragma unroll
+    for (int kk = 0; kk < KK / 2; ++kk)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) qturn[kk * 8 + e] = a.rope_turns[32 * kk + 8 * j4 + e];
+    const int kl = lane < PPR / 2 ? lane : 0;
+    krot_lo = *(const u32x4*)(knew + kl * 8);
+    krot_hi = *(const u32x4*)(knew + D / 2 + kl * 8);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) kturn[e] = a.rope_turns[8 * kl + e];
+  }
+
   // The group's query rows go to the wave's LDS query tile by the same DMA as K and V, ahead
   // of the first K/V loads, so the first step's vmcnt wait covers them too (rows of heads
   // >= G repeat head G-1 and are zeroed when read).
-  {
+  if constexpr (!ROPE) {
     const uint16_t* qbase = (const uint16_t*)a.q + ((size_t)b * a.hq + (size_t)g * G) * D;
 #pragma unroll
     for (int x = 0; x < 16 / RPI; ++x) {
@@ -391,6 +414,19 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
   auto compute = [&](const unsigned char* tile, int step) {
     // This step's tiles have landed once at most the next step's OPS loads are outstanding.
     __builtin_amdgcn_s_waitcnt(0x0F70 | (OPS & 15) | ((OPS >> 4) << 14));
+    if constexpr (ROPE) {
+      // The current token's K row arrived unrotated from k_new: overwrite it with the turned
+      // key before the tile is read.
+      if (step == (R.n_ring >> 5)) {
+        const int rc = R.n_ring & 31;
+        if (lane < PPR / 2) {
+          unsigned char* row = (unsigned char*)tile + rc * ROWB;
+          *(u32x4*)(row + ((lane ^ kswz(rc)) << 4)) = krot_lo;
+          *(u32x4*)(row + (((lane + PPR / 2) ^ kswz(rc)) << 4)) = krot_hi;
+        }
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      }
+    }
     const int k0 = step * 32;
     f32x4 s0 = {0.0f, 0.0f, 0.0f, 0.0f};
     f32x4 s1 = {0.0f, 0.0f, 0.0f, 0.0f};
@@ -456,8 +492,40 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
   // Queries: wait until at most the two prefetched steps are outstanding, then read the
   // B operand (channels 32kk + 8j .. +7 of head c16; zero for padded heads).
   __builtin_amdgcn_s_waitcnt(0x0F70 | ((2 * OPS) & 15) | (((2 * OPS) >> 4) << 14));
+  if constexpr (ROPE) {
+    // Turn the queries (channel 32kk + 8j + e pairs with the same channel of slice kk + KK/2)
+    // and the new key; round to bf16 as the matrix-core operands and the ring hold them.
+    const u32x4 zero = {0u, 0u, 0u, 0u};
 #pragma unroll
-  for (int kk = 0; kk < KK; ++kk) {
+    for (int kk = 0; kk < KK / 2; ++kk) {
+      bf16x8 x = __builtin_bit_cast(bf16x8, qraw[kk]);
+      bf16x8 y = __builtin_bit_cast(bf16x8, qraw[kk + KK / 2]);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        float cs, sn, ox, oy;
+        rope_cos_sin(t, qturn[kk * 8 + e], cs, sn);
+        rope_turn((float)x[e], (float)y[e], cs, sn, ox, oy);
+        x[e] = (__bf16)ox;
+        y[e] = (__bf16)oy;
+      }
+      qB[kk] = c16 < G ? x : __builtin_bit_cast(bf16x8, zero);
+      qB[kk + KK / 2] = c16 < G ? y : __builtin_bit_cast(bf16x8, zero);
+    }
+    bf16x8 x = __builtin_bit_cast(bf16x8, krot_lo);
+    bf16x8 y = __builtin_bit_cast(bf16x8, krot_hi);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      float cs, sn, ox, oy;
+      rope_cos_sin(t, kturn[e], cs, sn);
+      rope_turn((float)x[e], (float)y[e], cs, sn, ox, oy);
+      x[e] = (__bf16)ox;
+      y[e] = (__bf16)oy;
+    }
+    krot_lo = __builtin_bit_cast(u32x4, x);
+    krot_hi = __builtin_bit_cast(u32x4, y);
+  }
+#pragma unroll
+  for (int kk = 0; kk < (ROPE ? 0 : KK); ++kk) {
     const u32x4 zero = {0u, 0u, 0u, 0u};
     const u32x4 w = *(const u32x4*)(qtile + c16 * ROWB + (4 * kk + j4) * 16);
     qB[kk] = __builtin_bit_cast(bf16x8, c16 < G ? w : zero);
@@ -518,9 +586,18 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
 
   // Fused append of the current token.  Slot t mod slots holds a position outside the support
   // of t (and of every later step), so no read of this launch can observe the write.
-  if (appender)
+  if constexpr (ROPE) {
+    if (wave == 0 && lane < PPR / 2) {
+      uint16_t* dst = kring + (size_t)R.append_slot * D;
+      *(u32x4*)(dst + lane * 8) = krot_lo;
+      *(u32x4*)(dst + D / 2 + lane * 8) = krot_hi;
+    }
+    if (appender && lane >= PPR)
+      *(u32x4*)(vring + (size_t)R.append_slot * D + (lane % PPR) * 8) = append_row;
+  } else if (appender) {
     *(u32x4*)((lane < PPR ? kring : vring) + (size_t)R.append_slot * D + (lane % PPR) * 8) =
         append_row;
+  }
 }
 
 }  // namespace
@@ -556,10 +633,14 @@ hipError_t launch_ring_fill(const int32_t* pos, const void* k_src, const void* v
 template <int D, int NW>
 void launch_bf16_policy(const DecodeArgs& a, bool nt, hipStream_t stream) {
   const dim3 grid((unsigned)(a.batch * a.hkv));
-  if (nt)
-    hipLaunchKernelGGL((decode_bf16_kernel<D, NW, true>), grid, dim3(NW * 64), 0, stream, a);
-  else
-    hipLaunchKernelGGL((decode_bf16_kernel<D, NW, false>), grid, dim3(NW * 64), 0, stream, a);
+  const dim3 block(NW * 64);
+  if (a.rope) {
+    if (nt) hipLaunchKernelGGL((decode_bf16_kernel<D, NW, true, true>), grid, block, 0, stream, a);
+    else hipLaunchKernelGGL((decode_bf16_kernel<D, NW, false, true>), grid, block, 0, stream, a);
+  } else {
+    if (nt) hipLaunchKernelGGL((decode_bf16_kernel<D, NW, true, false>), grid, block, 0, stream, a);
+    else hipLaunchKernelGGL((decode_bf16_kernel<D, NW, false, false>), grid, block, 0, stream, a);
+  }
 }
 
 hipError_t launch_decode_bf16(const DecodeArgs& a, int32_t head_dim, hipStream_t stream) {

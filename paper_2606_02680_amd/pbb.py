@@ -38,7 +38,8 @@ class PbbDesc(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("n_q_heads", ctypes.c_int32),
                 ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
                 ("block", ctypes.c_int32), ("window", ctypes.c_int32),
-                ("slots", ctypes.c_int32), ("dtype", ctypes.c_int32), ("scale", ctypes.c_float)]
+                ("slots", ctypes.c_int32), ("dtype", ctypes.c_int32), ("scale", ctypes.c_float),
+                ("rope_base", ctypes.c_float)]
 
     @property
     def torch_dtype(self) -> torch.dtype:
@@ -88,14 +89,15 @@ def lib_status_string(status: int) -> str:
 
 def make_desc(batch: int, n_q_heads: int, n_kv_heads: int, head_dim: int, *, block: int = 0,
               window: int = 0, slots: int | None = None, dtype=torch.bfloat16,
-              scale: float = 0.0) -> PbbDesc:
+              scale: float = 0.0, rope_base: float = 0.0) -> PbbDesc:
     """Descriptor for a PBB ring (``block`` = B, ``slots`` = B) or, with ``window`` > 0, an SWA
-    ring (``slots`` >= ``window``, default ``window``)."""
+    ring (``slots`` >= ``window``, default ``window``).  ``rope_base`` > 1 makes the decode
+    steps apply the rotary embedding to q and k_new themselves (see ``include/pbb.h``)."""
     if slots is None:
         slots = window if window > 0 else block
     code = {torch.float32: DTYPE_F32, torch.bfloat16: DTYPE_BF16}.get(dtype, dtype)
     return PbbDesc(batch, n_q_heads, n_kv_heads, head_dim, block, window, slots, int(code),
-                   float(scale))
+                   float(scale), float(rope_base))
 
 
 def _stream(stream):

@@ -20,8 +20,10 @@ def desc_for(cfg: W.Config, batch: int | None = None) -> P.PbbDesc:
     dt = torch.float32 if cfg.dtype == "f32" else torch.bfloat16
     b = cfg.batch if batch is None else batch
     if cfg.mode == "swa":
-        return P.make_desc(b, cfg.hq, cfg.hkv, cfg.d, window=cfg.window, slots=cfg.slots, dtype=dt)
-    return P.make_desc(b, cfg.hq, cfg.hkv, cfg.d, block=cfg.block, dtype=dt)
+        return P.make_desc(b, cfg.hq, cfg.hkv, cfg.d, window=cfg.window, slots=cfg.slots, dtype=dt,
+                           rope_base=cfg.rope_base)
+    return P.make_desc(b, cfg.hq, cfg.hkv, cfg.d, block=cfg.block, dtype=dt,
+                       rope_base=cfg.rope_base)
 
 
 def bf16_tolerance_ok(got: np.ndarray, ref: np.ndarray):
@@ -88,6 +90,12 @@ class Run:
             self.hist_len = self.desc.slots
             ks = W.kv_window(self.cfg, "k", self.t0, self.hist_len, device=self.device)
             vs = W.kv_window(self.cfg, "v", self.t0, self.hist_len, device=self.device)
+            if self.cfg.rope_base:
+                # A rotary decode leaves rotated keys in the ring: fill it with the prefix keys
+                # turned by their positions (fp64 rotation, rounded to bf16).
+                posm = self.t0.view(-1, 1, 1) + torch.arange(-self.hist_len, 0).view(1, 1, -1)
+                rot = oracle.rope_rows(to_np(ks), posm.numpy(), self.cfg.rope_base)
+                ks = torch.from_numpy(rot).to(ks.dtype).to(self.device)
             P.ring_fill(self.desc, self.pos, ks, vs, self.k_ring, self.v_ring)
             del ks, vs
         self.seq = torch.arange(self.t0.numel(), dtype=torch.int64)
@@ -132,7 +140,8 @@ class Run:
         pos = (self.t0.numpy()[rows] + step).astype(np.int64)
         mode = oracle.SWA if self.cfg.mode == "swa" else oracle.PBB
         return oracle.decode(mode, pos, to_np(q[torch.as_tensor(rows, device=q.device)]), to_np(kh), to_np(vh), lo,
-                             block=self.cfg.block, window=self.cfg.window)
+                             block=self.cfg.block, window=self.cfg.window,
+                             rope_base=self.cfg.rope_base)
 
     def expected_ring(self, rows: np.ndarray, step: int, which: str, hist=None):
         """Bit pattern the ring must hold after ``step`` (0-based) has run."""
@@ -141,6 +150,18 @@ class Run:
         t_last = self.t0.numpy()[rows] + step
         first = np.maximum(0, self.t0.numpy()[rows] - self.hist_len)
         return oracle.expected_ring(bits(h), lo, t_last, first, self.desc.slots)
+
+    def expected_rotated_keys(self, rows: np.ndarray, step: int, hist=None) -> np.ndarray:
+        """fp64 image of the K ring of a rotary run after ``step``: every slot holds the exact
+        rotation of its key (or the initial zeros)."""
+        kh, vh, lo = self.history(rows, step) if hist is None else hist
+        posm = lo.reshape(-1, 1, 1) + np.arange(kh.shape[2]).reshape(1, 1, -1)
+        rot = oracle.rope_rows(to_np(kh), posm, self.cfg.rope_base)
+        t_last = self.t0.numpy()[rows] + step
+        first = np.maximum(0, self.t0.numpy()[rows] - self.hist_len)
+        return oracle.expected_ring(rot, lo, t_last, first, self.desc.slots,
+                                    initial=np.zeros((len(rows),) + rot.shape[1:2] +
+                                                     (self.desc.slots, rot.shape[3])))
 
     def ring_rows(self, rows: np.ndarray, which: str) -> np.ndarray:
         r = self.k_ring if which == "k" else self.v_ring

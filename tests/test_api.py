@@ -208,3 +208,12 @@ def test_prefill_argument_errors(fn):
     bad = _desc(window=65, slots=64) if fn == "swa_prefill" else _desc(block=63, slots=63)
     assert _prefill(bad, fn) == 2
     assert _prefill(desc, fn, n=0) == 0                   # nothing to do, nothing launched
+
+
+def test_rope_descriptor_rules():
+    assert _decode(_desc(rope_base=0.5)) == 2                   # bases in (0, 1] are rejected
+    assert _decode(_desc(rope_base=float("nan"))) == 2
+    assert _decode(_desc(rope_base=-1.0)) == 2
+    assert _decode(_desc(rope_base=1e6, dtype=B.DTYPE_F32)) == 3  # rotary decode is bf16 only
+    assert _prefill(_desc(rope_base=1e6)) == 2                   # prefill takes rotated inputs
+    assert _decode(_desc(rope_base=1e6), q=A + 2) == 4           # other checks unchanged

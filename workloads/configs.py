@@ -28,6 +28,7 @@ class Config:
     spike_prob: float = 0.0   # probability that a (sequence, position) has K and V scaled
     spike_scale: float = 1.0  # the scale applied to spiked positions
     prefill: bool = False     # rings hold the history before the first position
+    rope_base: float = 0.0    # > 0: decode applies rotary positions with this base
 
     @property
     def group(self) -> int:
