@@ -88,10 +88,11 @@ class Workload:
         dt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
         if cfg.mode == "swa":
             self.desc = P.make_desc(cfg.batch, cfg.hq, cfg.hkv, cfg.d, window=cfg.window,
-                                    slots=cfg.slots, dtype=dt)
+                                    slots=cfg.slots, dtype=dt, rope_base=cfg.rope_base)
             self.fn = P.swa_decode_step
         else:
-            self.desc = P.make_desc(cfg.batch, cfg.hq, cfg.hkv, cfg.d, block=cfg.block, dtype=dt)
+            self.desc = P.make_desc(cfg.batch, cfg.hq, cfg.hkv, cfg.d, block=cfg.block, dtype=dt,
+                                    rope_base=cfg.rope_base)
             self.fn = P.pbb_decode_step
         self.k_ring, self.v_ring = P.alloc_rings(self.desc, device)
         self.ws = P.alloc_workspace(self.desc, device)
@@ -424,6 +425,15 @@ def main(argv=None):
                            "pbb_over_swa_tokens_per_s": value / (cfg.batch * ext_steps / el)}
             del sw
             torch.cuda.empty_cache()
+        # The same step with the rotary embedding fused in (q and the new key turned by position,
+        # base 10^6): timing only, so the pre-filled ring is not re-rotated.
+        rw = Workload(cfg.with_(rope_base=1e6), t0, n_steps, device, inputs=inputs)
+        el, ks, tb = rw.timed(args.warmup, ext_steps)
+        extra["c3_rope_base1e6"] = {"tokens_per_s": cfg.batch * ext_steps / el,
+                                    "kernel_us": ks * 1e6,
+                                    "hbm_gbps_kernel": tb / ext_steps / ks / 1e9,
+                                    "kernel_us_over_plain": ks / kern_s}
+        del rw
         del inputs
         torch.cuda.empty_cache()
         c4 = W.get_config("c4")
