@@ -17,6 +17,8 @@ Layers?"):
   ``s mod b``; :func:`expected_ring` gives the ring image that sequential appends produce.
 * Appendix C -- rotary positions with base 10^6 (RoPE); half-split channel pairs as in the
   Qwen2.5 decoders the paper trains (:func:`rope`, ``decode(..., rope_base=...)``).
+* Sec. 3 (the fused kernel's backward propagation; Appendix F.4, grouped backward checks) --
+  :func:`backward`, the gradients of the prefill attention with respect to q, k, v.
 * Appendix A.4, Eq.(lse) -- the log-partition ``log sum_s e^{z_s}`` that :func:`prefill` also
   returns for every prompt position (the quantity a tiled prefill rescales with).
 
@@ -84,6 +86,9 @@ def _load():
     lib.oracle_decode_rope.argtypes = [i32, i64, i64, i64, i64, i64, i64, vp, vp, vp, vp, vp,
                                        i64, dbl, dbl, vp, i32]
     lib.oracle_decode_rope.restype = i32
+    lib.oracle_backward.argtypes = [i32, i64, i64, i64, i64, i64, i64, i64, vp, vp, vp, vp, dbl,
+                                    vp, vp, vp, i32]
+    lib.oracle_backward.restype = i32
     lib.oracle_prefill.argtypes = [i32, i64, i64, i64, i64, i64, i64, i64, vp, vp, vp, dbl, vp,
                                    vp, i32]
     lib.oracle_prefill.restype = i32
@@ -248,6 +253,30 @@ def prefill(mode: int, q, k, v, *, block: int = 0, window: int = 0, scale: float
     if rc != 0:
         raise ValueError("oracle.prefill: invalid arguments")
     return out, lse
+
+
+def backward(mode: int, q, k, v, dout, *, block: int = 0, window: int = 0,
+             scale: float | None = None, n_threads: int = 0):
+    """Gradients of :func:`prefill`'s output with respect to q, k, v for the upstream gradient
+    ``dout`` ([batch][n][Hq][d]), fp64: returns ``(dq, dk, dv)`` shaped like q, k, v."""
+    q = np.ascontiguousarray(q, dtype=np.float32)
+    k = np.ascontiguousarray(k, dtype=np.float32)
+    v = np.ascontiguousarray(v, dtype=np.float32)
+    dout = np.ascontiguousarray(dout, dtype=np.float32)
+    batch, n, hq, d = q.shape
+    assert dout.shape == q.shape and k.shape == v.shape and k.shape[:2] == (batch, n)
+    hkv = k.shape[2]
+    if scale is None:
+        scale = 1.0 / np.sqrt(d)
+    dq = np.zeros(q.shape, dtype=np.float64)
+    dk = np.zeros(k.shape, dtype=np.float64)
+    dv = np.zeros(v.shape, dtype=np.float64)
+    rc = _load().oracle_backward(int(mode), batch, n, hq, hkv, d, int(block), int(window),
+                                 _ptr(q), _ptr(k), _ptr(v), _ptr(dout), float(scale), _ptr(dq),
+                                 _ptr(dk), _ptr(dv), int(n_threads))
+    if rc != 0:
+        raise ValueError("oracle.backward: invalid arguments")
+    return dq, dk, dv
 
 
 # ----------------------------------------------------------------------------------------

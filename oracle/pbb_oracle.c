@@ -13,6 +13,7 @@
  *   - the sliding-window support {max(0,t-w+1)..t}                         Prop. 2 (Sec. 2.2)
  *   - single-softmax attention over a support, scores q.k/sqrt(d)          Sec. 3, Eq.(attention)
  *   - rotary positions (RoPE, base 10^6 in the paper's models), half-split pairs  Appendix C
+ *   - backward: gradients of the prefill attention w.r.t. q, k, v        Sec. 3; App. F.4
  *   - prefill: every prompt position over its own support, with its log-partition
  *     log sum_s e^{z_s}                                                    Appendix A.4, Eq.(lse)
  * Keys and values are read from HISTORY arrays indexed by absolute position, never from
@@ -458,6 +459,156 @@ int oracle_prefill(int mode, int64_t batch, int64_t n, int64_t n_q_heads, int64_
     if (n_threads > 256) n_threads = 256;
     pthread_t th[256];
     for (int i = 0; i < n_threads; ++i) pthread_create(&th[i], NULL, prefill_worker, &j);
+    for (int i = 0; i < n_threads; ++i) pthread_join(th[i], NULL);
+    pthread_mutex_destroy(&j.lock);
+    return 0;
+}
+
+/* ------------------------------------------------------------------------------------ */
+/* Backward of the prefill attention (training): gradients of q, k, v.                   */
+
+typedef struct {
+    int mode;
+    int64_t batch, n, n_q_heads, n_kv_heads, head_dim, block, window;
+    const float *q, *k, *v, *dout; /* q, dout [batch][n][Hq][d]; k, v [batch][n][Hkv][d] */
+    double scale;
+    double *dq, *dk, *dv; /* dq [batch][n][Hq][d]; dk, dv [batch][n][Hkv][d] */
+    int64_t next;
+    pthread_mutex_t lock;
+} backward_job;
+
+static int backward_member(const backward_job *j, int64_t t, int64_t s) {
+    if (j->mode == 0) return oracle_pbb_member(t, s, j->block, j->block / 2);
+    return oracle_swa_member(t, s, j->window);
+}
+
+/*
+ * All query heads of one (sequence, KV head) pair, every position t.  With o = sum_s p_s v_s,
+ * p_s = e^{z_s} / sum_u e^{z_u}, z_s = scale q.k_s over the support A(t) (Eq.(attention)) and an
+ * upstream gradient g = dL/do:
+ *   dL/dv_s += p_s g;   dL/dp_s = g.v_s;   dL/dz_s = p_s (g.v_s - g.o);
+ *   dL/dq += scale sum_s dL/dz_s k_s;   dL/dk_s += scale dL/dz_s q.
+ * Query heads of the KV head add into the same dk, dv (grouped-query attention).
+ */
+static void backward_one(backward_job *j, int64_t item, double *z, double *o, double *qd,
+                         double *gd) {
+    const int64_t d = j->head_dim, hq = j->n_q_heads, hkv = j->n_kv_heads, n = j->n;
+    const int64_t G = hq / hkv;
+    const int64_t b = item / hkv, g = item % hkv;
+    const int64_t span = (j->mode == 0) ? (j->block + j->block / 2) : j->window;
+    for (int64_t i = g * G; i < (g + 1) * G; ++i) {
+        for (int64_t t = 0; t < n; ++t) {
+            int64_t lo = t - span;
+            if (lo < 0) lo = 0;
+            for (int64_t c = 0; c < d; ++c) {
+                qd[c] = (double)j->q[((b * n + t) * hq + i) * d + c];
+                gd[c] = (double)j->dout[((b * n + t) * hq + i) * d + c];
+                o[c] = 0.0;
+            }
+            double m = -INFINITY;
+            for (int64_t s = lo; s <= t; ++s) {
+                if (!backward_member(j, t, s)) continue;
+                const float *ks = j->k + ((b * n + s) * hkv + g) * d;
+                double acc = 0.0;
+                for (int64_t c = 0; c < d; ++c) acc += qd[c] * (double)ks[c];
+                z[s - lo] = acc * j->scale;
+                if (z[s - lo] > m) m = z[s - lo];
+            }
+            double den = 0.0;
+            for (int64_t s = lo; s <= t; ++s) {
+                if (!backward_member(j, t, s)) continue;
+                z[s - lo] = exp(z[s - lo] - m);
+                den += z[s - lo];
+            }
+            for (int64_t s = lo; s <= t; ++s) {
+                if (!backward_member(j, t, s)) continue;
+                z[s - lo] /= den; /* p_s */
+                const float *vs = j->v + ((b * n + s) * hkv + g) * d;
+                for (int64_t c = 0; c < d; ++c) o[c] += z[s - lo] * (double)vs[c];
+            }
+            double go = 0.0;
+            for (int64_t c = 0; c < d; ++c) go += gd[c] * o[c];
+            double *dqt = j->dq + ((b * n + t) * hq + i) * d;
+            for (int64_t s = lo; s <= t; ++s) {
+                if (!backward_member(j, t, s)) continue;
+                const double p = z[s - lo];
+                const float *ks = j->k + ((b * n + s) * hkv + g) * d;
+                const float *vs = j->v + ((b * n + s) * hkv + g) * d;
+                double gv = 0.0;
+                for (int64_t c = 0; c < d; ++c) gv += gd[c] * (double)vs[c];
+                const double dz = p * (gv - go);
+                double *dks = j->dk + ((b * n + s) * hkv + g) * d;
+                double *dvs = j->dv + ((b * n + s) * hkv + g) * d;
+                for (int64_t c = 0; c < d; ++c) {
+                    dvs[c] += p * gd[c];
+                    dqt[c] += j->scale * dz * (double)ks[c];
+                    dks[c] += j->scale * dz * qd[c];
+                }
+            }
+        }
+    }
+}
+
+static void *backward_worker(void *arg) {
+    backward_job *j = (backward_job *)arg;
+    const int64_t span = (j->mode == 0) ? (j->block + j->block / 2) : j->window;
+    double *z = (double *)malloc(sizeof(double) * (size_t)(span + 1));
+    double *buf = (double *)malloc(sizeof(double) * (size_t)(3 * j->head_dim));
+    const int64_t total = j->batch * j->n_kv_heads;
+    for (;;) {
+        pthread_mutex_lock(&j->lock);
+        int64_t item = j->next;
+        j->next += 1;
+        pthread_mutex_unlock(&j->lock);
+        if (item >= total) break;
+        backward_one(j, item, z, buf, buf + j->head_dim, buf + 2 * j->head_dim);
+    }
+    free(z);
+    free(buf);
+    return NULL;
+}
+
+/*
+ * Gradients of the prefill attention (positions 0..n-1, support Eq.(pbb) with h = block/2 when
+ * mode == 0, Prop. 2 when mode == 1) for an upstream gradient dout of the output: dq, dk, dv in
+ * fp64, zero-initialised here.  Layouts as oracle_prefill; dk, dv [batch][n][Hkv][d].
+ * Returns 0, or 2 on bad arguments.
+ */
+int oracle_backward(int mode, int64_t batch, int64_t n, int64_t n_q_heads, int64_t n_kv_heads,
+                    int64_t head_dim, int64_t block, int64_t window, const float *q,
+                    const float *k, const float *v, const float *dout, double scale, double *dq,
+                    double *dk, double *dv, int n_threads) {
+    if (batch < 0 || n < 0 || n_q_heads <= 0 || n_kv_heads <= 0 || head_dim <= 0) return 2;
+    if (n_q_heads % n_kv_heads != 0) return 2;
+    if (mode == 0 && (block < 2 || block % 2 != 0)) return 2;
+    if (mode == 1 && window < 1) return 2;
+    memset(dq, 0, sizeof(double) * (size_t)(batch * n * n_q_heads * head_dim));
+    memset(dk, 0, sizeof(double) * (size_t)(batch * n * n_kv_heads * head_dim));
+    memset(dv, 0, sizeof(double) * (size_t)(batch * n * n_kv_heads * head_dim));
+    backward_job j;
+    memset(&j, 0, sizeof(j));
+    j.mode = mode;
+    j.batch = batch;
+    j.n = n;
+    j.n_q_heads = n_q_heads;
+    j.n_kv_heads = n_kv_heads;
+    j.head_dim = head_dim;
+    j.block = block;
+    j.window = window;
+    j.q = q;
+    j.k = k;
+    j.v = v;
+    j.dout = dout;
+    j.scale = scale;
+    j.dq = dq;
+    j.dk = dk;
+    j.dv = dv;
+    pthread_mutex_init(&j.lock, NULL);
+    if (n_threads <= 0) n_threads = (int)sysconf(_SC_NPROCESSORS_ONLN);
+    if (n_threads < 1) n_threads = 1;
+    if (n_threads > 256) n_threads = 256;
+    pthread_t th[256];
+    for (int i = 0; i < n_threads; ++i) pthread_create(&th[i], NULL, backward_worker, &j);
     for (int i = 0; i < n_threads; ++i) pthread_join(th[i], NULL);
     pthread_mutex_destroy(&j.lock);
     return 0;
