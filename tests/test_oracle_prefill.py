@@ -153,8 +153,8 @@ PREFILL_MUTATIONS = {
                     "    const int64_t g = i % hkv;\n    double *o = j->out + ((b * n + t)"),
     "bridge_dropped": ("if (j->mode == 0) return oracle_pbb_member(t, s, j->block, j->block / 2);\n    return oracle_swa_member(t, s, j->window);\n}\n\n/* One (sequence, position",
                        "if (j->mode == 0) return oracle_pbb_member(t, s, j->block, 0);\n    return oracle_swa_member(t, s, j->window);\n}\n\n/* One (sequence, position"),
-    "value_row_off_by_one": ("const float *vs = j->v + ((b * n + s) * hkv + g) * d;",
-                             "const float *vs = j->v + ((b * n + (s > 0 ? s - 1 : s)) * hkv + g) * d;"),
+    "value_row_off_by_one": ("const float *vs = j->v + ((b * n + s) * hkv + g) * d;\n        double w = exp",
+                             "const float *vs = j->v + ((b * n + (s > 0 ? s - 1 : s)) * hkv + g) * d;\n        double w = exp"),
 }
 
 
