@@ -9,7 +9,7 @@ Default workload (c3): batch 256, Hq 32, Hkv 8, head_dim 128, B 2048, bf16, posi
 uniform in [0, 512K).  Also reported: the same-library sliding-window ring on the same
 tensors (W = 2B = 4096 in 4096 slots, plus the paper-matched W = B), the ragged GQA-8
 workload (c4), the paper-shape latency sweep, and prefill (PBB and SWA) in TFLOP/s against
-the bf16 matrix-core peak.
+the bf16 matrix-core peak, and the training backward of the same shapes.
 
 Prints ONE JSON line.  Roofline: algorithmic bytes of the support actually read (ring K and
 V rows of |A(t)| - 1 sources, q, out, the new K/V and their slot write, pos) divided by the
@@ -211,6 +211,57 @@ def prefill_extras(device):
     return res
 
 
+def backward_measure(device, batch, n, hq, hkv, d, block=0, window=0, reps=10):
+    """Median time of one backward call (delta, dq and dk/dv launches; HIP events on the launch
+    stream) after a prefill supplied ``out`` and ``lse``; algorithmic rate
+    10 * d * Hq * batch * sum_t |A(t)| FLOP (the five products per covered pair: scores,
+    dout.v, dq, dk, dv; the kernels recompute the first two once more in the dk/dv pass)."""
+    import torch
+    import paper_2606_02680_amd as P
+    import workloads as W
+    mode = "pbb" if block else "swa"
+    cfg = W.Config(f"backward-{mode}", mode, batch=batch, hq=hq, hkv=hkv, d=d, block=block,
+                   slots=block or window, window=window, dtype="bf16", seed=7, value_scale=1.0,
+                   pos_hi=0, steps=1)
+    q, k, v = W.prompt(cfg, n, device=device)
+    dout, _, _ = W.prompt(cfg.with_(seed=8), n, device=device)
+    if block:
+        desc = P.make_desc(batch, hq, hkv, d, block=block, dtype=torch.bfloat16)
+        fwd, bwd = P.pbb_prefill, P.pbb_backward
+    else:
+        desc = P.make_desc(batch, hq, hkv, d, window=window, slots=window, dtype=torch.bfloat16)
+        fwd, bwd = P.swa_prefill, P.swa_backward
+    out = torch.empty_like(q)
+    lse = torch.empty((batch, hq, n), dtype=torch.float32, device=device)
+    stream = torch.cuda.current_stream()
+    fwd(desc, q, k, v, out, lse, stream=stream)
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    ws = torch.empty(P.backward_workspace_bytes(desc, n), dtype=torch.uint8, device=device)
+    for _ in range(2):
+        bwd(desc, q, k, v, out, dout, lse, dq, dk, dv, workspace=ws, stream=stream)
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(reps)]
+    for e0, e1 in ev:
+        e0.record(stream)
+        bwd(desc, q, k, v, out, dout, lse, dq, dk, dv, workspace=ws, stream=stream)
+        e1.record(stream)
+    torch.cuda.synchronize()
+    ms = sorted(e0.elapsed_time(e1) for e0, e1 in ev)[reps // 2]
+    flops = 10.0 * d * hq * batch * prefill_support_total(n, block, window)
+    tflops = flops / (ms * 1e-3) / 1e12
+    return {"ms": ms, "tflops": tflops, "frac_of_bf16_mfma_peak": tflops / MFMA_BF16_PEAK_TFLOPS,
+            "tokens_per_s": batch * n / (ms * 1e-3), "algorithmic_tflop": flops / 1e12}
+
+
+BACKWARD_SHAPES = tuple((name.replace("prefill", "backward"), shape)
+                        for name, shape in PREFILL_SHAPES)
+
+
+def backward_extras(device):
+    return {name: backward_measure(device, **shape) for name, shape in BACKWARD_SHAPES}
+
+
 PAPER_ORIGINS = (8192, 16384, 32768, 65536, 131072, 262144, 524288, 1048576)
 
 
@@ -329,6 +380,8 @@ def main(argv=None):
                     help="only run the paper-shape latency sweep (3 shapes x 8 origins)")
     ap.add_argument("--prefill", action="store_true",
                     help="only run the prefill measurements (c3 head shapes and paper shape)")
+    ap.add_argument("--backward", action="store_true",
+                    help="only run the training-backward measurements (same shapes as prefill)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only time a plain 1 GiB device copy (HBM counter calibration)")
     args = ap.parse_args(argv)
@@ -363,6 +416,10 @@ def main(argv=None):
 
     if args.prefill:
         print(json.dumps({"prefill": prefill_extras(device)}), flush=True)
+        return 0
+
+    if args.backward:
+        print(json.dumps({"backward": backward_extras(device)}), flush=True)
         return 0
 
     if args.paper_latency:
@@ -450,6 +507,7 @@ def main(argv=None):
         extra["paper_shape_latency_us_per_step"] = paper_latency(
             device, shapes=(10, 12, 14), origins=(8192, 1048576))
         extra["prefill"] = prefill_extras(device)
+        extra["backward"] = backward_extras(device)
         result["extra"] = extra
         result["paper_context"] = ("Flash-PBB 1.82x Flash-SWA decode-core throughput on an RTX "
                                    "4090 (48 GB), BF16, batch 1, Hkv 2, d 64, b 128 vs w 128")

@@ -198,6 +198,37 @@ pbb_status_t swa_prefill(const pbb_desc_t *desc, int32_t n, const void *q, const
                          const void *v, void *out, float *lse, void *k_ring, void *v_ring,
                          void *stream);
 
+/*
+ * Training backward of the prefill attention: gradients with respect to q, k, v for an
+ * upstream gradient dout of the prefill output (the paper's fused kernel includes backward
+ * propagation, Sec. 3, and its grouped backward sums the query heads of a KV head, Appendix
+ * F.4).  With p_s = exp(z_s - lse_t) over A(t) and delta_t = dout_t . out_t:
+ *   dv_s += p_s dout_t,  dq_t = scale sum_s p_s (dout_t.v_s - delta_t) k_s,
+ *   dk_s += scale p_s (dout_t.v_s - delta_t) q_t,
+ * summed over the query heads of each KV head for dk and dv.
+ *   q, out, dout, dq   [batch][n][n_q_heads][head_dim]   (out: the prefill output)
+ *   k, v, dk, dv       [batch][n][n_kv_heads][head_dim]
+ *   lse                float32 [batch][n_q_heads][n], the prefill's log-partitions
+ * bfloat16 only; fp32 accumulation, gradients rounded RNE; every gradient element is written
+ * once (no accumulation into the outputs; deterministic).  Requires rope_base == 0 (inputs
+ * already rotated) and 0 <= n <= 2^30; n == 0 does nothing.  Alignment as pbb_prefill.
+ * workspace: device memory of pbb_backward_workspace_bytes bytes (16-byte aligned, contents
+ * irrelevant; holds delta); PBB_ERR_WORKSPACE if NULL or smaller.  Enqueues three kernels on
+ * the stream.  The gradient buffers must not alias the inputs.
+ */
+pbb_status_t pbb_backward_workspace_bytes(const pbb_desc_t *desc, int32_t n, size_t *bytes);
+
+pbb_status_t pbb_backward(const pbb_desc_t *desc, int32_t n, const void *q, const void *k,
+                          const void *v, const void *out, const void *dout, const float *lse,
+                          void *dq, void *dk, void *dv, void *workspace, size_t workspace_bytes,
+                          void *stream);
+
+/* Sliding-window counterpart of pbb_backward (support of Prop. 2; SWA descriptor rules). */
+pbb_status_t swa_backward(const pbb_desc_t *desc, int32_t n, const void *q, const void *k,
+                          const void *v, const void *out, const void *dout, const float *lse,
+                          void *dq, void *dk, void *dv, void *workspace, size_t workspace_bytes,
+                          void *stream);
+
 #ifdef __cplusplus
 }
 #endif

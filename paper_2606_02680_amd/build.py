@@ -1,7 +1,8 @@
 """Build libpbb.so in-tree with hipcc for gfx950.
 
 ``python -m paper_2606_02680_amd.build`` compiles ``csrc/pbb_api.cpp``,
-``csrc/pbb_kernels.hip`` (decode) and ``csrc/pbb_prefill.hip`` (prefill) into ``paper_2606_02680_amd/libpbb.so`` and writes the compiler's
+``csrc/pbb_kernels.hip`` (decode), ``csrc/pbb_prefill.hip`` (prefill) and
+``csrc/pbb_backward.hip`` (training backward) into ``paper_2606_02680_amd/libpbb.so`` and writes the compiler's
 per-kernel resource report (VGPRs, AGPRs, SGPRs, LDS, scratch) to ``csrc/resource_usage.txt``.
 """
 from __future__ import annotations
@@ -33,7 +34,7 @@ def hipcc() -> str:
 
 def build(verbose: bool = False) -> str:
     sources = [os.path.join(CSRC, "pbb_api.cpp"), os.path.join(CSRC, "pbb_kernels.hip"),
-               os.path.join(CSRC, "pbb_prefill.hip")]
+               os.path.join(CSRC, "pbb_prefill.hip"), os.path.join(CSRC, "pbb_backward.hip")]
     tmp = LIB + ".tmp"
     cmd = [hipcc(), *HIPCC_FLAGS, "-Rpass-analysis=kernel-resource-usage", *sources, "-o", tmp]
     proc = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)

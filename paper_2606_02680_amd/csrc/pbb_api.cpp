@@ -150,6 +150,61 @@ pbb_status_t prefill_common(const pbb_desc_t* desc, bool swa, int32_t n, const v
   return e == hipSuccess ? PBB_OK : PBB_ERR_LAUNCH;
 }
 
+size_t backward_workspace(const pbb_desc_t* d, int32_t n) {
+  const size_t f = (size_t)d->batch * (size_t)d->n_q_heads * (size_t)(n > 0 ? n : 0) * 4;
+  return (f + 255) / 256 * 256;
+}
+
+pbb_status_t backward_common(const pbb_desc_t* desc, bool swa, int32_t n, const void* q,
+                             const void* k, const void* v, const void* out, const void* dout,
+                             const float* lse, void* dq, void* dk, void* dv, void* workspace,
+                             size_t workspace_bytes, void* stream) {
+  const pbb_status_t st = check_desc(desc, swa);
+  if (st != PBB_OK) return st;
+  if (desc->dtype != PBB_DTYPE_BF16) return PBB_ERR_DTYPE;
+  if (desc->rope_base != 0.0f) return PBB_ERR_SHAPE;  // rotated inputs, as for prefill
+  if (n < 0 || n > kMaxPrefill) return PBB_ERR_SHAPE;
+  if (!q || !k || !v || !out || !dout || !lse || !dq || !dk || !dv) return PBB_ERR_NULL;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16) ||
+      !aligned(dout, 16) || !aligned(dq, 16) || !aligned(dk, 16) || !aligned(dv, 16) ||
+      !aligned(lse, 4))
+    return PBB_ERR_ALIGN;
+  if ((uint64_t)desc->batch * (uint64_t)desc->n_kv_heads * ((uint64_t)n / 4 + 1) > 0x7fffffffull)
+    return PBB_ERR_SHAPE;
+  // the delta launch covers 16 (d = 128) or 32 rows of batch x n x Hq per workgroup
+  if ((uint64_t)desc->batch * (uint64_t)desc->n_q_heads * (uint64_t)n / 16 + 1 > 0x7fffffffull)
+    return PBB_ERR_SHAPE;
+  if (n == 0) return PBB_OK;
+  if (workspace == nullptr || workspace_bytes < backward_workspace(desc, n))
+    return PBB_ERR_WORKSPACE;
+  if (!aligned(workspace, 16)) return PBB_ERR_ALIGN;
+
+  pbb::BackwardArgs a;
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.out = out;
+  a.dout = dout;
+  a.lse = lse;
+  a.dq = dq;
+  a.dk = dk;
+  a.dv = dv;
+  a.delta = static_cast<float*>(workspace);
+  a.batch = desc->batch;
+  a.n = n;
+  a.hq = desc->n_q_heads;
+  a.hkv = desc->n_kv_heads;
+  a.group = desc->n_q_heads / desc->n_kv_heads;
+  a.mode = swa ? pbb::kSupportSWA : pbb::kSupportPBB;
+  a.block = desc->block;
+  a.window = desc->window;
+  a.scale = desc->scale > 0.0f ? desc->scale : (float)(1.0 / std::sqrt((double)desc->head_dim));
+  a.scale_log2 = (float)((double)a.scale * 1.4426950408889634);
+  const hipError_t e =
+      pbb::launch_backward_bf16(a, desc->head_dim, reinterpret_cast<hipStream_t>(stream));
+  return e == hipSuccess ? PBB_OK : PBB_ERR_LAUNCH;
+}
+
 }  // namespace
 
 extern "C" {
@@ -259,6 +314,31 @@ pbb_status_t swa_prefill(const pbb_desc_t* desc, int32_t n, const void* q, const
                          const void* v, void* out, float* lse, void* k_ring, void* v_ring,
                          void* stream) {
   return prefill_common(desc, true, n, q, k, v, out, lse, k_ring, v_ring, stream);
+}
+
+pbb_status_t pbb_backward_workspace_bytes(const pbb_desc_t* desc, int32_t n, size_t* bytes) {
+  if (desc == nullptr || bytes == nullptr) return PBB_ERR_NULL;
+  const pbb_status_t st = check_desc(desc, is_swa(desc));
+  if (st != PBB_OK) return st;
+  if (n < 0 || n > kMaxPrefill) return PBB_ERR_SHAPE;
+  *bytes = backward_workspace(desc, n);
+  return PBB_OK;
+}
+
+pbb_status_t pbb_backward(const pbb_desc_t* desc, int32_t n, const void* q, const void* k,
+                          const void* v, const void* out, const void* dout, const float* lse,
+                          void* dq, void* dk, void* dv, void* workspace, size_t workspace_bytes,
+                          void* stream) {
+  return backward_common(desc, false, n, q, k, v, out, dout, lse, dq, dk, dv, workspace,
+                         workspace_bytes, stream);
+}
+
+pbb_status_t swa_backward(const pbb_desc_t* desc, int32_t n, const void* q, const void* k,
+                          const void* v, const void* out, const void* dout, const float* lse,
+                          void* dq, void* dk, void* dv, void* workspace, size_t workspace_bytes,
+                          void* stream) {
+  return backward_common(desc, true, n, q, k, v, out, dout, lse, dq, dk, dv, workspace,
+                         workspace_bytes, stream);
 }
 
 }  // extern "C"

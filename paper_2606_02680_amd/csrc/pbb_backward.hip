@@ -1,0 +1,555 @@
+// HIP backward of the PBB (and SWA) prefill attention on gfx950: gradients of q, k, v for
+// training (the paper's fused kernel includes backward propagation, Sec. 3; its grouped backward
+// sums the gradients of the query heads that share a KV head, Appendix F.4).
+//
+// For target t with support A(t), p_s = exp(z_s - lse_t), z_s = scale q_t.k_s (Eq.(attention);
+// lse_t the forward's log-partition, Appendix A.4 Eq.(lse)) and upstream gradient g_t:
+//   dv_s += p_s g_t
+//   ds_s  = p_s (g_t.v_s - delta_t),   delta_t = g_t.o_t
+//   dq_t  = scale sum_s ds_s k_s,      dk_s += scale ds_s q_t
+// summed over the query heads of each KV head for dk and dv.  Three launches:
+//   delta: one fp32 dot product per (sequence, head, position) into the workspace;
+//   dq:    the prefill kernel's structure (64 query columns per workgroup walk their key
+//          interval in 32-key steps through LDS), no running maximum (lse is known);
+//   dk/dv: transposed roles: each workgroup holds 64 keys of one KV head in registers and
+//          walks, for every query head of the group, the interval of targets whose supports
+//          contain those keys (PBB: up to h(floor(s/h) + 2) - 1; SWA: s + W - 1).
+// Every gradient element is written once, by the one workgroup that owns it (no atomics,
+// deterministic).  Matrix-core products use v_mfma_f32_16x16x32_bf16 with the score layout of
+// the forward (16 B-operand columns, 32 rows in two halves), P and dS rounded to bf16 as
+// operands, fp32 accumulation, bf16 (RNE) outputs.
+
+#include <type_traits>
+
+#include "pbb_device.h"
+#include "pbb_internal.h"
+
+namespace pbb {
+namespace {
+
+constexpr int kBwdWaves = 4;
+
+// Tiles read both as matrix-core row operands (16 bytes of one row per lane) and through
+// transposed reads (4 rows x 32 bytes per 16 lanes) store 16-byte piece p of row r at
+// p ^ g(r); g spreads both access patterns over all banks.
+template <int D>
+__device__ __forceinline__ int dual_swz(int r) {
+  if constexpr (D == 128) return (2 * (r & 3)) | ((r >> 2) & 1) | (((r >> 3) & 1) << 3);
+  return (2 * (r & 3)) | ((r >> 2) & 1);
+}
+
+// ------------------------------------------------------------------------------------------
+// delta = dout . out, one 16-lane (d = 128) or 8-lane (d = 64) group per row.
+template <int D>
+__global__ __launch_bounds__(256) void bwd_delta_kernel(BackwardArgs a) {
+  constexpr int PPR = D / 8;
+  const size_t rows = (size_t)a.batch * a.n * a.hq;
+  const size_t row = (size_t)blockIdx.x * (256 / PPR) + threadIdx.x / PPR;
+  const int p = threadIdx.x % PPR;
+  float acc = 0.0f;
+  if (row < rows) {
+    const bf16x8 g = *(const bf16x8*)((const uint16_t*)a.dout + row * D + p * 8);
+    const bf16x8 o = *(const bf16x8*)((const uint16_t*)a.out + row * D + p * 8);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc = __builtin_fmaf((float)g[e], (float)o[e], acc);
+  }
+#pragma unroll
+  for (int m = PPR / 2; m >= 1; m >>= 1) acc += __shfl_xor(acc, m);
+  if (row < rows && p == 0) {
+    const size_t h = row % a.hq;
+    const size_t bt = row / a.hq;
+    const size_t t = bt % a.n;
+    const size_t b = bt / a.n;
+    a.delta[(b * a.hq + h) * a.n + t] = acc;
+  }
+}
+
+// Workgroup i runs on XCD i mod 8: give each XCD a contiguous run of tiles.
+__device__ __forceinline__ int xcd_tile() {
+  const int nblk = gridDim.x;
+  const int per = nblk >> 3, rem = nblk & 7;
+  const int xcd = blockIdx.x & 7, local = blockIdx.x >> 3;
+  return (xcd < rem ? xcd * (per + 1) : rem * (per + 1) + (xcd - rem) * per) + local;
+}
+
+// ------------------------------------------------------------------------------------------
+// dq: 64 query columns (TQ positions x G heads, position-major) per workgroup, 16 per wave.
+template <int D>
+__global__ __launch_bounds__(kBwdWaves * 64) __attribute__((amdgpu_waves_per_eu(2)))
+void bwd_dq_kernel(BackwardArgs a, int tq, int tiles) {
+  constexpr int NW = kBwdWaves;
+  constexpr int KK = D / 32, NB = D / 16, ROWB = D * 2, PPR = D / 8, RPI = 64 / PPR;
+  constexpr int NG = 32 / RPI;
+  constexpr int TILE = 32 * ROWB;
+  constexpr int BUF = 2 * TILE;          // K tile (dual layout), V tile (dual layout)
+  constexpr int STAGES = 3;
+  constexpr int OPS = 2 * NG;
+  constexpr int MYOPS = OPS / NW;
+  static_assert(OPS % NW == 0, "DMA split");
+  __shared__ __align__(16) unsigned char smem[STAGES * BUF];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int c16 = lane & 15, j4 = lane >> 4;
+  const int G = a.group, n = a.n;
+  const int tile_id = xcd_tile();
+  const int bg = tile_id / tiles, tile = tile_id - bg * tiles;
+  const int b = bg / a.hkv, g = bg - b * a.hkv;
+  const int t0 = tile * tq;
+  const int t_last = min(n - 1, t0 + tq - 1);
+  const int kbeg = support_start(a.mode, a.block, a.window, t0);
+  const int s_first = kbeg >> 5;
+  const int nsteps = (t_last >> 5) - s_first + 1;
+  const int mask_lo = support_start(a.mode, a.block, a.window, t_last);
+  const int mask_hi = t0;
+
+  const size_t rowstride = (size_t)a.hkv * ROWB;
+  const unsigned char* kbase = (const unsigned char*)a.k + ((size_t)b * n * a.hkv + g) * ROWB;
+  const unsigned char* vbase = (const unsigned char*)a.v + ((size_t)b * n * a.hkv + g) * ROWB;
+
+  // This lane's query column: position t0 + col / G, head g*G + col % G.
+  const int col = wave * 16 + c16;
+  const int cp = col / G;
+  const int tc = t0 + cp;
+  const int hc = g * G + (col - cp * G);
+  const bool valid = cp < tq && tc < n;
+  const int lo_c = valid ? support_start(a.mode, a.block, a.window, tc) : 0x7fffffff;
+  const int hi_c = valid ? tc : -1;
+  bf16x8 qB[KK], gB[KK];
+  {
+    const size_t rowq = ((size_t)b * n + (valid ? tc : t0)) * a.hq + hc;
+    const uint16_t* qrow = (const uint16_t*)a.q + rowq * D;
+    const uint16_t* grow = (const uint16_t*)a.dout + rowq * D;
+    const u32x4 zero = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      const u32x4 wq = *(const u32x4*)(qrow + 32 * kk + 8 * j4);
+      const u32x4 wg = *(const u32x4*)(grow + 32 * kk + 8 * j4);
+      qB[kk] = __builtin_bit_cast(bf16x8, valid ? wq : zero);
+      gB[kk] = __builtin_bit_cast(bf16x8, valid ? wg : zero);
+    }
+  }
+  const size_t lrow = ((size_t)b * a.hq + hc) * n + (valid ? tc : t0);
+  const float lse2 = valid ? a.lse[lrow] * 1.4426950408889634f : 0.0f;
+  const float dlt = valid ? a.delta[lrow] : 0.0f;
+
+  // DMA of one step (K then V rows of keys 32*(s_first+st) ..), clamped to t_last.
+  const unsigned char* src[MYOPS];
+  int row_of[MYOPS];
+#pragma unroll
+  for (int o = 0; o < MYOPS; ++o) {
+    const int op = wave * MYOPS + o;
+    const bool isv = op >= NG;
+    const int x = isv ? op - NG : op;
+    const int row = x * RPI + lane / PPR;
+    const int piece = (lane % PPR) ^ dual_swz<D>(row);
+    row_of[o] = row;
+    src[o] = (isv ? vbase : kbase) + (size_t)(s_first * 32 + row) * rowstride + piece * 16;
+  }
+  const size_t step_bytes = 32 * rowstride;
+  auto issue = [&](int stage, int st) {
+    unsigned char* tp = smem + stage * BUF;
+    const bool tail = (s_first + st) * 32 + 31 > t_last;
+#pragma unroll
+    for (int o = 0; o < MYOPS; ++o) {
+      const int op = wave * MYOPS + o;
+      const bool isv = op >= NG;
+      const int x = isv ? op - NG : op;
+      const unsigned char* s = src[o] + (size_t)st * step_bytes;
+      if (tail) {
+        const int over = (s_first + st) * 32 + row_of[o] - t_last;
+        if (over > 0) s -= (size_t)over * rowstride;
+      }
+      __builtin_amdgcn_global_load_lds(
+          (const void*)s, (__attribute__((address_space(3))) void*)(tp + (isv ? TILE : 0) + x * 1024),
+          16, 0, 0);
+    }
+  };
+
+  // Transposed-read addresses of this lane in stage 0 (K tile), chunk nb: row 4j + c/4,
+  // channels 16nb + 4(c mod 4) .. +3.
+  uint32_t kaddr[NB];
+  {
+    const uint32_t base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) unsigned char*)smem;
+    const int r = 4 * j4 + (c16 >> 2);
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      const int p = 2 * nb + ((c16 & 3) >> 1);
+      kaddr[nb] = base + r * ROWB + ((p ^ dual_swz<D>(r)) << 4) + ((c16 & 1) << 3);
+    }
+  }
+
+  f32x4 acc[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+  const float c = a.scale_log2;
+
+  issue(0, 0);
+  if (nsteps > 1) issue(1, 1);
+
+  auto step = [&](int st, auto masked) {
+    if (st + 1 < nsteps)
+      __builtin_amdgcn_s_waitcnt(0x0F70 | (MYOPS & 15) | ((MYOPS >> 4) << 14));
+    else
+      __builtin_amdgcn_s_waitcnt(0x0F70);
+    lds_barrier();
+    if (st + 2 < nsteps) issue((st + 2) % STAGES, st + 2);
+    __builtin_amdgcn_sched_barrier(0);
+    const unsigned char* kt = smem + (st % STAGES) * BUF;
+    const unsigned char* vt = kt + TILE;
+    const int k0 = (s_first + st) * 32;
+    f32x4 s0 = {0.0f, 0.0f, 0.0f, 0.0f}, s1 = s0, d0 = s0, d1 = s0;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      const int p = 4 * kk + j4;
+      const bf16x8 ka = *(const bf16x8*)(kt + c16 * ROWB + ((p ^ dual_swz<D>(c16)) << 4));
+      const bf16x8 kb =
+          *(const bf16x8*)(kt + (16 + c16) * ROWB + ((p ^ dual_swz<D>(16 + c16)) << 4));
+      const bf16x8 va = *(const bf16x8*)(vt + c16 * ROWB + ((p ^ dual_swz<D>(c16)) << 4));
+      const bf16x8 vb =
+          *(const bf16x8*)(vt + (16 + c16) * ROWB + ((p ^ dual_swz<D>(16 + c16)) << 4));
+      s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qB[kk], s0, 0, 0, 0);
+      s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb, qB[kk], s1, 0, 0, 0);
+      d0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, gB[kk], d0, 0, 0, 0);
+      d1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vb, gB[kk], d1, 0, 0, 0);
+    }
+    // ds = p (dp - delta), p = exp2(s c - lse2); masked keys give p = 0.
+    bf16x8 dsB;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float sc = e < 4 ? s0[e] : s1[e - 4];
+      const float dp = e < 4 ? d0[e] : d1[e - 4];
+      float pe = fast_exp2(__builtin_fmaf(sc, c, -lse2));
+      if constexpr (decltype(masked)::value) {
+        const int key = k0 + (e < 4 ? 4 * j4 + e : 16 + 4 * j4 + (e - 4));
+        pe = (key >= lo_c && key <= hi_c) ? pe : 0.0f;
+      }
+      dsB[e] = (__bf16)(pe * (dp - dlt));
+    }
+    // dq^T += K^T ds^T: the K^T operand by transposed reads of the K tile.
+    const uint32_t sb = (uint32_t)((st % STAGES) * BUF);
+    u32x2 kr[2 * NB];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      kr[2 * nb] = tr_read<0>(kaddr[nb] + sb);
+      kr[2 * nb + 1] = tr_read<16 * ROWB>(kaddr[nb] + sb);
+    }
+    if constexpr (NB == 8) {
+      asm volatile("s_waitcnt lgkmcnt(0)"
+                   : "+v"(kr[0]), "+v"(kr[1]), "+v"(kr[2]), "+v"(kr[3]), "+v"(kr[4]),
+                     "+v"(kr[5]), "+v"(kr[6]), "+v"(kr[7]), "+v"(kr[8]), "+v"(kr[9]),
+                     "+v"(kr[10]), "+v"(kr[11]), "+v"(kr[12]), "+v"(kr[13]), "+v"(kr[14]),
+                     "+v"(kr[15]));
+    } else {
+      asm volatile("s_waitcnt lgkmcnt(0)"
+                   : "+v"(kr[0]), "+v"(kr[1]), "+v"(kr[2]), "+v"(kr[3]), "+v"(kr[4]),
+                     "+v"(kr[5]), "+v"(kr[6]), "+v"(kr[7]));
+    }
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      const u32x4 w = {kr[2 * nb][0], kr[2 * nb][1], kr[2 * nb + 1][0], kr[2 * nb + 1][1]};
+      acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, w), dsB,
+                                                        acc[nb], 0, 0, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  int st_a = (mask_lo + 31) / 32 - s_first;
+  int st_b = (mask_hi + 1) / 32 - s_first;
+  st_a = max(0, min(st_a, nsteps));
+  st_b = max(st_a, min(st_b, nsteps));
+  for (int st = 0; st < st_a; ++st) step(st, std::true_type{});
+  for (int st = st_a; st < st_b; ++st) step(st, std::false_type{});
+  for (int st = st_b; st < nsteps; ++st) step(st, std::true_type{});
+
+  if (valid) {
+    uint16_t* drow = (uint16_t*)a.dq + (((size_t)b * n + tc) * a.hq + hc) * D;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      u32x2 w;
+      w[0] = (uint32_t)float_to_bf16_rne(acc[nb][0] * a.scale) |
+             ((uint32_t)float_to_bf16_rne(acc[nb][1] * a.scale) << 16);
+      w[1] = (uint32_t)float_to_bf16_rne(acc[nb][2] * a.scale) |
+             ((uint32_t)float_to_bf16_rne(acc[nb][3] * a.scale) << 16);
+      *(u32x2*)(drow + 16 * nb + 4 * j4) = w;
+    }
+  }
+}
+
+// ------------------------------------------------------------------------------------------
+// dk, dv: 64 keys of one KV head per workgroup (16 per wave, held as matrix-core B operands);
+// the workgroup walks (query head, 32-target step) pairs through LDS: Q and dout rows (dual
+// layout) and the steps' lse and delta values.
+template <int D>
+__global__ __launch_bounds__(kBwdWaves * 64) __attribute__((amdgpu_waves_per_eu(2)))
+void bwd_dkdv_kernel(BackwardArgs a, int tiles) {
+  constexpr int NW = kBwdWaves;
+  constexpr int KK = D / 32, NB = D / 16, ROWB = D * 2, PPR = D / 8, RPI = 64 / PPR;
+  constexpr int NG = 32 / RPI;
+  constexpr int TILE = 32 * ROWB;
+  constexpr int BUF = 2 * TILE + 256;   // Q tile, dout tile, lse2[32] and delta[32]
+  constexpr int STAGES = 3;
+  constexpr int ROWOPS = 2 * NG;        // row DMAs per step; wave 0 also issues the lse/delta one
+  constexpr int MYOPS = ROWOPS / NW;
+  static_assert(ROWOPS % NW == 0, "DMA split");
+  constexpr int KT = 16 * NW;           // keys per workgroup
+  __shared__ __align__(16) unsigned char smem[STAGES * BUF];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int c16 = lane & 15, j4 = lane >> 4;
+  const int G = a.group, n = a.n;
+  const int tile_id = xcd_tile();
+  const int bg = tile_id / tiles, tile = tile_id - bg * tiles;
+  const int b = bg / a.hkv, g = bg - b * a.hkv;
+  const int s0k = tile * KT;                       // first key of the workgroup
+  const int s1k = min(n - 1, s0k + KT - 1);        // last key
+  const int q_first = s0k & ~31;                   // targets before s0k see none of these keys
+  const int q_end = min(n - 1, support_last_target(a.mode, a.block, a.window, s1k));
+  const int qsteps = (q_end >> 5) - (q_first >> 5) + 1;
+  const int nsteps = G * qsteps;                    // (head, target step) pairs
+
+  // This wave's keys as B operands: lane (key c16, slice j) holds channels 32kk + 8j .. +7.
+  const int key = s0k + wave * 16 + c16;
+  const bool kvalid = key < n;
+  bf16x8 kB[KK], vB[KK];
+  {
+    const size_t rowk = ((size_t)b * n + (kvalid ? key : s0k)) * a.hkv + g;
+    const uint16_t* krow = (const uint16_t*)a.k + rowk * D;
+    const uint16_t* vrow = (const uint16_t*)a.v + rowk * D;
+    const u32x4 zero = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      const u32x4 wk = *(const u32x4*)(krow + 32 * kk + 8 * j4);
+      const u32x4 wv = *(const u32x4*)(vrow + 32 * kk + 8 * j4);
+      kB[kk] = __builtin_bit_cast(bf16x8, kvalid ? wk : zero);
+      vB[kk] = __builtin_bit_cast(bf16x8, kvalid ? wv : zero);
+    }
+  }
+
+  // DMA of step gs: rows of head g*G + gs / qsteps, targets q_first + 32 (gs mod qsteps) ..
+  // (clamped to q_end); wave 0 also loads the 32 lse and 32 delta values (one 4-byte DMA).
+  const size_t qrowstride = (size_t)a.hq * ROWB;
+  auto issue = [&](int stage, int gs) {
+    unsigned char* tp = smem + stage * BUF;
+    const int hi = gs / qsteps;
+    const int head = g * G + hi;
+    const int q0 = q_first + 32 * (gs - hi * qsteps);
+#pragma unroll
+    for (int o = 0; o < MYOPS; ++o) {
+      const int op = wave * MYOPS + o;
+      const bool isg = op >= NG;
+      const int x = isg ? op - NG : op;
+      const int row = x * RPI + lane / PPR;
+      const int t = min(q0 + row, q_end);
+      const int piece = (lane % PPR) ^ dual_swz<D>(row);
+      const unsigned char* s = (const unsigned char*)(isg ? a.dout : a.q) +
+                               ((size_t)b * n + t) * qrowstride + (size_t)head * ROWB + piece * 16;
+      __builtin_amdgcn_global_load_lds(
+          (const void*)s, (__attribute__((address_space(3))) void*)(tp + (isg ? TILE : 0) + x * 1024),
+          16, 0, 0);
+    }
+    if (wave == 0) {
+      const int t = min(q0 + (lane & 31), q_end);
+      const float* s = (lane < 32 ? a.lse : a.delta) + ((size_t)b * a.hq + head) * n + t;
+      __builtin_amdgcn_global_load_lds((const void*)s,
+                                       (__attribute__((address_space(3))) void*)(tp + 2 * TILE),
+                                       4, 0, 0);
+    }
+  };
+
+  // Transposed-read addresses (stage 0) of the Q tile for chunk nb; the dout tile is TILE on.
+  uint32_t taddr[NB];
+  {
+    const uint32_t base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) unsigned char*)smem;
+    const int r = 4 * j4 + (c16 >> 2);
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      const int p = 2 * nb + ((c16 & 3) >> 1);
+      taddr[nb] = base + r * ROWB + ((p ^ dual_swz<D>(r)) << 4) + ((c16 & 1) << 3);
+    }
+  }
+
+  f32x4 acck[NB], accv[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    acck[nb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    accv[nb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+  }
+  const float c = a.scale_log2;
+  const float log2e = 1.4426950408889634f;
+
+  issue(0, 0);
+  if (nsteps > 1) issue(1, 1);
+
+  // Every (target, key) of a step is in the support when all its targets come after the
+  // workgroup's last key and the first key is at or after the support start of its last target.
+  auto step = [&](int gs, auto masked) {
+    if (wave == 0) {
+      if (gs + 1 < nsteps)
+        __builtin_amdgcn_s_waitcnt(0x0F70 | ((MYOPS + 1) & 15) | (((MYOPS + 1) >> 4) << 14));
+      else
+        __builtin_amdgcn_s_waitcnt(0x0F70);
+    } else {
+      if (gs + 1 < nsteps)
+        __builtin_amdgcn_s_waitcnt(0x0F70 | (MYOPS & 15) | ((MYOPS >> 4) << 14));
+      else
+        __builtin_amdgcn_s_waitcnt(0x0F70);
+    }
+    lds_barrier();
+    if (gs + 2 < nsteps) issue((gs + 2) % STAGES, gs + 2);
+    __builtin_amdgcn_sched_barrier(0);
+    const unsigned char* qt = smem + (gs % STAGES) * BUF;
+    const unsigned char* gt = qt + TILE;
+    const float* lt = (const float*)(qt + 2 * TILE);
+    const int hi = gs / qsteps;
+    const int q0 = q_first + 32 * (gs - hi * qsteps);
+    // Scores with targets on the rows (two halves of 16) and this wave's keys on the columns.
+    f32x4 s0 = {0.0f, 0.0f, 0.0f, 0.0f}, s1 = s0, d0 = s0, d1 = s0;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      const int p = 4 * kk + j4;
+      const bf16x8 qa = *(const bf16x8*)(qt + c16 * ROWB + ((p ^ dual_swz<D>(c16)) << 4));
+      const bf16x8 qb =
+          *(const bf16x8*)(qt + (16 + c16) * ROWB + ((p ^ dual_swz<D>(16 + c16)) << 4));
+      const bf16x8 ga = *(const bf16x8*)(gt + c16 * ROWB + ((p ^ dual_swz<D>(c16)) << 4));
+      const bf16x8 gb =
+          *(const bf16x8*)(gt + (16 + c16) * ROWB + ((p ^ dual_swz<D>(16 + c16)) << 4));
+      s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa, kB[kk], s0, 0, 0, 0);
+      s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qb, kB[kk], s1, 0, 0, 0);
+      d0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ga, vB[kk], d0, 0, 0, 0);
+      d1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gb, vB[kk], d1, 0, 0, 0);
+    }
+    // lse and delta of this lane's 8 targets (rows 4j..4j+3 and 16+4j..16+4j+3).
+    const f32x4 la = *(const f32x4*)(lt + 4 * j4);
+    const f32x4 lb = *(const f32x4*)(lt + 16 + 4 * j4);
+    const f32x4 da = *(const f32x4*)(lt + 32 + 4 * j4);
+    const f32x4 db = *(const f32x4*)(lt + 48 + 4 * j4);
+    bf16x8 pB, dsB;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float sc = e < 4 ? s0[e] : s1[e - 4];
+      const float dp = e < 4 ? d0[e] : d1[e - 4];
+      const float l2 = (e < 4 ? la[e] : lb[e - 4]) * log2e;
+      const float dl = e < 4 ? da[e] : db[e - 4];
+      float pe = fast_exp2(__builtin_fmaf(sc, c, -l2));
+      if constexpr (decltype(masked)::value) {
+        const int t = q0 + (e < 4 ? 4 * j4 + e : 16 + 4 * j4 + (e - 4));
+        const bool in = t <= q_end && key <= t &&
+                        key >= support_start(a.mode, a.block, a.window, t);
+        pe = in ? pe : 0.0f;
+      }
+      pB[e] = (__bf16)pe;
+      dsB[e] = (__bf16)(pe * (dp - dl));
+    }
+    // dv^T += dout^T p, dk^T += Q^T ds: dout^T and Q^T by transposed reads.
+    const uint32_t sb = (uint32_t)((gs % STAGES) * BUF);
+    u32x2 qr[2 * NB], gr[2 * NB];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      gr[2 * nb] = tr_read<TILE>(taddr[nb] + sb);
+      gr[2 * nb + 1] = tr_read<TILE + 16 * ROWB>(taddr[nb] + sb);
+    }
+    if constexpr (NB == 8) {
+      asm volatile("s_waitcnt lgkmcnt(0)"
+                   : "+v"(gr[0]), "+v"(gr[1]), "+v"(gr[2]), "+v"(gr[3]), "+v"(gr[4]),
+                     "+v"(gr[5]), "+v"(gr[6]), "+v"(gr[7]), "+v"(gr[8]), "+v"(gr[9]),
+                     "+v"(gr[10]), "+v"(gr[11]), "+v"(gr[12]), "+v"(gr[13]), "+v"(gr[14]),
+                     "+v"(gr[15]));
+    } else {
+      asm volatile("s_waitcnt lgkmcnt(0)"
+                   : "+v"(gr[0]), "+v"(gr[1]), "+v"(gr[2]), "+v"(gr[3]), "+v"(gr[4]),
+                     "+v"(gr[5]), "+v"(gr[6]), "+v"(gr[7]));
+    }
+    // The Q^T reads go out before the dv products so that they overlap them.
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      qr[2 * nb] = tr_read<0>(taddr[nb] + sb);
+      qr[2 * nb + 1] = tr_read<16 * ROWB>(taddr[nb] + sb);
+    }
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      const u32x4 w = {gr[2 * nb][0], gr[2 * nb][1], gr[2 * nb + 1][0], gr[2 * nb + 1][1]};
+      accv[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, w), pB,
+                                                         accv[nb], 0, 0, 0);
+    }
+    if constexpr (NB == 8) {
+      asm volatile("s_waitcnt lgkmcnt(0)"
+                   : "+v"(qr[0]), "+v"(qr[1]), "+v"(qr[2]), "+v"(qr[3]), "+v"(qr[4]),
+                     "+v"(qr[5]), "+v"(qr[6]), "+v"(qr[7]), "+v"(qr[8]), "+v"(qr[9]),
+                     "+v"(qr[10]), "+v"(qr[11]), "+v"(qr[12]), "+v"(qr[13]), "+v"(qr[14]),
+                     "+v"(qr[15]));
+    } else {
+      asm volatile("s_waitcnt lgkmcnt(0)"
+                   : "+v"(qr[0]), "+v"(qr[1]), "+v"(qr[2]), "+v"(qr[3]), "+v"(qr[4]),
+                     "+v"(qr[5]), "+v"(qr[6]), "+v"(qr[7]));
+    }
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      const u32x4 w = {qr[2 * nb][0], qr[2 * nb][1], qr[2 * nb + 1][0], qr[2 * nb + 1][1]};
+      acck[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, w), dsB,
+                                                         acck[nb], 0, 0, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  // Unmasked steps: targets t in [s1k, ...] whose support starts at or before s0k.
+  for (int gs = 0; gs < nsteps; ++gs) {
+    const int hi = gs / qsteps;
+    const int q0 = q_first + 32 * (gs - hi * qsteps);
+    const int qlast = q0 + 31;
+    const bool interior = q0 >= s1k && qlast <= q_end &&
+                          support_start(a.mode, a.block, a.window, qlast) <= s0k &&
+                          s0k + KT - 1 == s1k;
+    if (interior) step(gs, std::false_type{});
+    else step(gs, std::true_type{});
+  }
+
+  if (kvalid) {
+    const size_t rowk = ((size_t)b * n + key) * a.hkv + g;
+    uint16_t* dkrow = (uint16_t*)a.dk + rowk * D;
+    uint16_t* dvrow = (uint16_t*)a.dv + rowk * D;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      u32x2 wk, wv;
+      wk[0] = (uint32_t)float_to_bf16_rne(acck[nb][0] * a.scale) |
+              ((uint32_t)float_to_bf16_rne(acck[nb][1] * a.scale) << 16);
+      wk[1] = (uint32_t)float_to_bf16_rne(acck[nb][2] * a.scale) |
+              ((uint32_t)float_to_bf16_rne(acck[nb][3] * a.scale) << 16);
+      wv[0] = (uint32_t)float_to_bf16_rne(accv[nb][0]) |
+              ((uint32_t)float_to_bf16_rne(accv[nb][1]) << 16);
+      wv[1] = (uint32_t)float_to_bf16_rne(accv[nb][2]) |
+              ((uint32_t)float_to_bf16_rne(accv[nb][3]) << 16);
+      *(u32x2*)(dkrow + 16 * nb + 4 * j4) = wk;
+      *(u32x2*)(dvrow + 16 * nb + 4 * j4) = wv;
+    }
+  }
+}
+
+template <int D>
+hipError_t launch_backward_d(const BackwardArgs& a, hipStream_t stream) {
+  constexpr int PPR = D / 8;
+  const size_t rows = (size_t)a.batch * a.n * a.hq;
+  const size_t dblocks = (rows + (256 / PPR) - 1) / (256 / PPR);
+  hipLaunchKernelGGL((bwd_delta_kernel<D>), dim3((unsigned)dblocks), dim3(256), 0, stream, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int tq = (16 * kBwdWaves) / a.group;
+  const int qtiles = (a.n + tq - 1) / tq;
+  hipLaunchKernelGGL((bwd_dq_kernel<D>), dim3((unsigned)((size_t)a.batch * a.hkv * qtiles)),
+                     dim3(kBwdWaves * 64), 0, stream, a, tq, qtiles);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int ktiles = (a.n + 16 * kBwdWaves - 1) / (16 * kBwdWaves);
+  hipLaunchKernelGGL((bwd_dkdv_kernel<D>), dim3((unsigned)((size_t)a.batch * a.hkv * ktiles)),
+                     dim3(kBwdWaves * 64), 0, stream, a, ktiles);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_backward_bf16(const BackwardArgs& a, int32_t head_dim, hipStream_t stream) {
+  return head_dim == 128 ? launch_backward_d<128>(a, stream) : launch_backward_d<64>(a, stream);
+}
+
+}  // namespace pbb

@@ -49,4 +49,55 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
+// First source a(t) of the support of target t: PBB (mode 0) max(0, h(floor(t/h) - 1)) with
+// h = block/2 (Sec. 3 "Flash-PBB"), SWA max(0, t - window + 1) (Prop. 2).  Never decreases in t.
+__device__ __forceinline__ int support_start(int mode, int block, int window, int t) {
+  int lo;
+  if (mode == 0) {
+    const int h = block >> 1;
+    lo = h * (t / h - 1);
+  } else {
+    lo = t - window + 1;
+  }
+  return lo > 0 ? lo : 0;
+}
+
+// Last target whose support contains source s (the largest t with support_start(t) <= s):
+// PBB h(floor(s/h) + 2) - 1, SWA s + window - 1.
+__device__ __forceinline__ int support_last_target(int mode, int block, int window, int s) {
+  if (mode == 0) {
+    const int h = block >> 1;
+    return h * (s / h + 2) - 1;
+  }
+  return s + window - 1;
+}
+
+// Value of lane l ^ 16 and of lane l ^ 32 (gfx950 v_permlane16_swap / v_permlane32_swap with
+// both operands x: one result is the lane's own value, the other its partner's), on the VALU
+// instead of an LDS permute.
+__device__ __forceinline__ float max_xor16_32(float x) {
+  auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+
+__device__ __forceinline__ float sum_xor16_32(float x) {
+  auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
+// Transposed LDS read (gfx950 ds_read_b64_tr_b16) at addr + OFF.  Issued as inline asm: the
+// compiler cannot tell these reads apart from the LDS DMA still in flight and would otherwise
+// wait for every outstanding load before each of them.  The caller waits with an s_waitcnt
+// that takes the results as operands, so that nothing reads them earlier.
+template <int OFF>
+__device__ __forceinline__ u32x2 tr_read(uint32_t addr) {
+  u32x2 r;
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(OFF));
+  return r;
+}
+
 }  // namespace pbb

@@ -55,6 +55,30 @@ struct PrefillArgs {
   float scale_log2;
 };
 
+// Backward of the prefill attention (gradients of q, k, v), validated on the host.
+struct BackwardArgs {
+  const void* q;       // [batch][n][hq][d]
+  const void* k;       // [batch][n][hkv][d]
+  const void* v;
+  const void* out;     // forward output [batch][n][hq][d]
+  const void* dout;    // upstream gradient [batch][n][hq][d]
+  const float* lse;    // forward log-partitions (natural log) [batch][hq][n]
+  void* dq;            // [batch][n][hq][d]
+  void* dk;            // [batch][n][hkv][d]
+  void* dv;
+  float* delta;        // workspace: dout . out per (sequence, head, position) [batch][hq][n]
+  int32_t batch;
+  int32_t n;
+  int32_t hq;
+  int32_t hkv;
+  int32_t group;
+  int32_t mode;        // SupportMode
+  int32_t block;
+  int32_t window;
+  float scale;         // softmax scale
+  float scale_log2;    // scale times log2(e)
+};
+
 hipError_t launch_ring_zero(void* k_ring, void* v_ring, size_t bytes_per_tensor,
                             hipStream_t stream);
 
@@ -68,6 +92,9 @@ hipError_t launch_decode_bf16(const DecodeArgs& a, int32_t head_dim, hipStream_t
 
 // bf16 prefill on matrix cores; head_dim 64 or 128; n >= 1.
 hipError_t launch_prefill_bf16(const PrefillArgs& a, int32_t head_dim, hipStream_t stream);
+
+// bf16 backward on matrix cores: delta, then dq, then dk/dv; head_dim 64 or 128; n >= 1.
+hipError_t launch_backward_bf16(const BackwardArgs& a, int32_t head_dim, hipStream_t stream);
 
 // fp32 decode on vector ALUs; head_dim 64 or 128.
 hipError_t launch_decode_f32(const DecodeArgs& a, int32_t head_dim, hipStream_t stream);

@@ -34,40 +34,7 @@ constexpr int kPrefillColGroups = 2;   // 16-column groups per wave
 constexpr int kPrefillCols = 16 * kPrefillColGroups * kPrefillWaves;
 
 __device__ __forceinline__ int support_lo(const PrefillArgs& a, int t) {
-  if (a.mode == kSupportPBB) {
-    const int h = a.block >> 1;
-    const int lo = h * (t / h - 1);
-    return lo > 0 ? lo : 0;
-  }
-  const int lo = t - a.window + 1;
-  return lo > 0 ? lo : 0;
-}
-
-// Value of lane l ^ 16 and of lane l ^ 32 (gfx950 v_permlane16_swap / v_permlane32_swap with
-// both operands x: one result is the lane's own value, the other its partner's), on the VALU
-// instead of an LDS permute.
-__device__ __forceinline__ float max_xor16_32(float x) {
-  auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
-  auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
-}
-
-__device__ __forceinline__ float sum_xor16_32(float x) {
-  auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
-  auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
-}
-
-// Transposed LDS read (gfx950 ds_read_b64_tr_b16) at addr + OFF.  Issued as inline asm: the
-// compiler cannot tell these reads apart from the LDS DMA still in flight and would otherwise
-// wait for every outstanding load before each of them.  The caller waits with lds_wait_regs.
-template <int OFF>
-__device__ __forceinline__ u32x2 tr_read(uint32_t addr) {
-  u32x2 r;
-  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(OFF));
-  return r;
+  return support_start(a.mode, a.block, a.window, t);
 }
 
 template <int D, int QC>

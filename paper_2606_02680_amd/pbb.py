@@ -24,7 +24,8 @@ _TORCH_DTYPE = {DTYPE_F32: torch.float32, DTYPE_BF16: torch.bfloat16}
 
 EXPORTS = ("pbb_status_string", "pbb_ring_bytes", "pbb_ring_init", "pbb_ring_fill",
            "pbb_workspace_bytes", "pbb_decode_step", "swa_workspace_bytes", "swa_decode_step",
-           "pbb_decode_step_advance", "swa_decode_step_advance", "pbb_prefill", "swa_prefill")
+           "pbb_decode_step_advance", "swa_decode_step_advance", "pbb_prefill", "swa_prefill",
+           "pbb_backward_workspace_bytes", "pbb_backward", "swa_backward")
 
 
 class PbbError(RuntimeError):
@@ -77,6 +78,9 @@ def load_library(path: str = _LIB_PATH):
         getattr(lib, fn).argtypes = [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     for fn in ("pbb_prefill", "swa_prefill"):
         getattr(lib, fn).argtypes = [dp, i32, vp, vp, vp, vp, vp, vp, vp, vp]
+    lib.pbb_backward_workspace_bytes.argtypes = [dp, i32, ctypes.POINTER(sz)]
+    for fn in ("pbb_backward", "swa_backward"):
+        getattr(lib, fn).argtypes = [dp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     for fn in EXPORTS[1:]:
         getattr(lib, fn).restype = ctypes.c_int
     _lib = lib
@@ -266,6 +270,42 @@ def pbb_prefill(desc: PbbDesc, q, k, v, out, lse=None, k_ring=None, v_ring=None,
 def swa_prefill(desc: PbbDesc, q, k, v, out, lse=None, k_ring=None, v_ring=None, stream=None):
     """Sliding-window counterpart of :func:`pbb_prefill` (support of Prop. 2)."""
     return _prefill("swa_prefill", desc, q, k, v, out, lse, k_ring, v_ring, stream)
+
+
+def backward_workspace_bytes(desc: PbbDesc, n: int) -> int:
+    out = ctypes.c_size_t()
+    _check("pbb_backward_workspace_bytes", load_library().pbb_backward_workspace_bytes(
+        ctypes.byref(desc), int(n), ctypes.byref(out)))
+    return out.value
+
+
+def _backward(fn: str, desc: PbbDesc, q, k, v, out, dout, lse, dq, dk, dv, workspace, stream):
+    n = q.shape[1]
+    for name, t in (("q", q), ("out", out), ("dout", dout), ("dq", dq)):
+        _expect(name, t, (desc.batch, n, desc.n_q_heads, desc.head_dim), desc.torch_dtype)
+    for name, t in (("k", k), ("v", v), ("dk", dk), ("dv", dv)):
+        _expect(name, t, (desc.batch, n, desc.n_kv_heads, desc.head_dim), desc.torch_dtype)
+    _expect("lse", lse, (desc.batch, desc.n_q_heads, n), torch.float32)
+    if workspace is None:
+        workspace = torch.empty(max(1, backward_workspace_bytes(desc, n)), dtype=torch.uint8,
+                                device=q.device)
+    ws_bytes = workspace.numel() * workspace.element_size()
+    _check(fn, getattr(load_library(), fn)(
+        ctypes.byref(desc), int(n), _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(dout), _ptr(lse),
+        _ptr(dq), _ptr(dk), _ptr(dv), _ptr(workspace), ctypes.c_size_t(ws_bytes), _stream(stream)))
+    return dq, dk, dv
+
+
+def pbb_backward(desc: PbbDesc, q, k, v, out, dout, lse, dq, dk, dv, workspace=None, stream=None):
+    """Gradients (dq, dk, dv) of :func:`pbb_prefill`'s output for the upstream gradient
+    ``dout``; ``out`` and ``lse`` are the prefill's outputs.  Allocates the workspace when none
+    is given."""
+    return _backward("pbb_backward", desc, q, k, v, out, dout, lse, dq, dk, dv, workspace, stream)
+
+
+def swa_backward(desc: PbbDesc, q, k, v, out, dout, lse, dq, dk, dv, workspace=None, stream=None):
+    """Sliding-window counterpart of :func:`pbb_backward`."""
+    return _backward("swa_backward", desc, q, k, v, out, dout, lse, dq, dk, dv, workspace, stream)
 
 
 def default_scale(head_dim: int) -> float:

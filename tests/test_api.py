@@ -217,3 +217,33 @@ def test_rope_descriptor_rules():
     assert _decode(_desc(rope_base=1e6, dtype=B.DTYPE_F32)) == 3  # rotary decode is bf16 only
     assert _prefill(_desc(rope_base=1e6)) == 2                   # prefill takes rotated inputs
     assert _decode(_desc(rope_base=1e6), q=A + 2) == 4           # other checks unchanged
+
+
+def _backward(desc, fn="pbb_backward", n=64, **ptrs):
+    args = dict(q=A, k=A, v=A, out=A, dout=A, lse=A, dq=A, dk=A, dv=A, ws=A, ws_bytes=1 << 20)
+    args.update(ptrs)
+    vp = ctypes.c_void_p
+    return getattr(B.load_library(), fn)(
+        ctypes.byref(desc), n, vp(args["q"]), vp(args["k"]), vp(args["v"]), vp(args["out"]),
+        vp(args["dout"]), vp(args["lse"]), vp(args["dq"]), vp(args["dk"]), vp(args["dv"]),
+        vp(args["ws"]), ctypes.c_size_t(args["ws_bytes"]), vp(0))
+
+
+@pytest.mark.parametrize("fn", ["pbb_backward", "swa_backward"])
+def test_backward_argument_errors(fn):
+    desc = _desc(window=32, slots=64) if fn == "swa_backward" else _desc()
+    for name in ("q", "k", "v", "out", "dout", "lse", "dq", "dk", "dv"):
+        assert _backward(desc, fn, **{name: 0}) == 1, name
+    for name in ("q", "k", "v", "out", "dout", "dq", "dk", "dv"):
+        assert _backward(desc, fn, **{name: A + 8}) == 4, name
+    assert _backward(desc, fn, lse=A + 2) == 4
+    need = P.backward_workspace_bytes(desc, 64)
+    assert need == 2 * 8 * 64 * 4          # batch x Hq x n floats (256-byte multiple)
+    assert _backward(desc, fn, ws=0) == 5
+    assert _backward(desc, fn, ws_bytes=need - 1) == 5
+    assert _backward(desc, fn, ws=A + 4, ws_bytes=need) == 4
+    assert _backward(desc, fn, n=-1) == 2
+    f32 = _desc(window=32, slots=64, dtype=B.DTYPE_F32) if fn == "swa_backward" else _desc(dtype=B.DTYPE_F32)
+    assert _backward(f32, fn) == 3
+    assert _backward(_desc(rope_base=1e6), "pbb_backward") == 2
+    assert _backward(desc, fn, n=0, ws=0) == 0
