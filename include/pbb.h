@@ -211,9 +211,11 @@ pbb_status_t swa_prefill(const pbb_desc_t *desc, int32_t n, const void *q, const
  *   lse                float32 [batch][n_q_heads][n], the prefill's log-partitions
  * bfloat16 only; fp32 accumulation, gradients rounded RNE; every gradient element is written
  * once (no accumulation into the outputs; deterministic).  Requires rope_base == 0 (inputs
- * already rotated) and 0 <= n <= 2^30; n == 0 does nothing.  Alignment as pbb_prefill.
- * workspace: device memory of pbb_backward_workspace_bytes bytes (16-byte aligned, contents
- * irrelevant; holds delta); PBB_ERR_WORKSPACE if NULL or smaller.  Enqueues three kernels on
+ * already rotated), 0 <= n <= 2^30 (n == 0 does nothing) and n_q_heads * head_dim <= 2^24
+ * (PBB_ERR_SHAPE otherwise).  Alignment as pbb_prefill.
+ * workspace: device memory of pbb_backward_workspace_bytes bytes = 8 * batch * n_q_heads * n
+ * rounded up to a multiple of 256 (16-byte aligned, contents irrelevant; holds lse * log2(e)
+ * and delta per position); PBB_ERR_WORKSPACE if NULL or smaller.  Enqueues three kernels on
  * the stream.  The gradient buffers must not alias the inputs.
  */
 pbb_status_t pbb_backward_workspace_bytes(const pbb_desc_t *desc, int32_t n, size_t *bytes);

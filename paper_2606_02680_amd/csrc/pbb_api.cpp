@@ -151,7 +151,7 @@ pbb_status_t prefill_common(const pbb_desc_t* desc, bool swa, int32_t n, const v
 }
 
 size_t backward_workspace(const pbb_desc_t* d, int32_t n) {
-  const size_t f = (size_t)d->batch * (size_t)d->n_q_heads * (size_t)(n > 0 ? n : 0) * 4;
+  const size_t f = (size_t)d->batch * (size_t)d->n_q_heads * (size_t)(n > 0 ? n : 0) * 8;
   return (f + 255) / 256 * 256;
 }
 
@@ -171,6 +171,8 @@ pbb_status_t backward_common(const pbb_desc_t* desc, bool swa, int32_t n, const 
     return PBB_ERR_ALIGN;
   if ((uint64_t)desc->batch * (uint64_t)desc->n_kv_heads * ((uint64_t)n / 4 + 1) > 0x7fffffffull)
     return PBB_ERR_SHAPE;
+  // 32 rows of one tensor lie within 32-bit byte offsets of the first
+  if ((uint64_t)desc->n_q_heads * (uint64_t)desc->head_dim > (1u << 24)) return PBB_ERR_SHAPE;
   // the delta launch covers 16 (d = 128) or 32 rows of batch x n x Hq per workgroup
   if ((uint64_t)desc->batch * (uint64_t)desc->n_q_heads * (uint64_t)n / 16 + 1 > 0x7fffffffull)
     return PBB_ERR_SHAPE;
@@ -189,7 +191,7 @@ pbb_status_t backward_common(const pbb_desc_t* desc, bool swa, int32_t n, const 
   a.dq = dq;
   a.dk = dk;
   a.dv = dv;
-  a.delta = static_cast<float*>(workspace);
+  a.ws = static_cast<float*>(workspace);
   a.batch = desc->batch;
   a.n = n;
   a.hq = desc->n_q_heads;

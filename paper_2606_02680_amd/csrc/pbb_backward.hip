@@ -27,7 +27,9 @@
 namespace pbb {
 namespace {
 
-constexpr int kBwdWaves = 4;
+// Waves per workgroup of the dq and dk/dv launches (16 query columns or 16 keys per wave).
+constexpr int kDqWaves = 4;
+constexpr int kDkdvWaves = 4;
 
 // Tiles read both as matrix-core row operands (16 bytes of one row per lane) and through
 // transposed reads (4 rows x 32 bytes per 16 lanes) store 16-byte piece p of row r at
@@ -39,7 +41,9 @@ __device__ __forceinline__ int dual_swz(int r) {
 }
 
 // ------------------------------------------------------------------------------------------
-// delta = dout . out, one 16-lane (d = 128) or 8-lane (d = 64) group per row.
+// Per (sequence, head, position): lse * log2(e) and delta = dout . out, into the workspace laid
+// out [batch][hq][2][n] (the two values of one (sequence, head) n floats apart).  One 16-lane
+// (d = 128) or 8-lane (d = 64) group per row.
 template <int D>
 __global__ __launch_bounds__(256) void bwd_delta_kernel(BackwardArgs a) {
   constexpr int PPR = D / 8;
@@ -60,7 +64,9 @@ __global__ __launch_bounds__(256) void bwd_delta_kernel(BackwardArgs a) {
     const size_t bt = row / a.hq;
     const size_t t = bt % a.n;
     const size_t b = bt / a.n;
-    a.delta[(b * a.hq + h) * a.n + t] = acc;
+    float* w = a.ws + (b * a.hq + h) * 2 * (size_t)a.n;
+    w[t] = a.lse[(b * a.hq + h) * a.n + t] * 1.4426950408889634f;
+    w[a.n + t] = acc;
   }
 }
 
@@ -72,20 +78,25 @@ __device__ __forceinline__ int xcd_tile() {
   return (xcd < rem ? xcd * (per + 1) : rem * (per + 1) + (xcd - rem) * per) + local;
 }
 
+// Issue of one 16-byte LDS DMA from a wave-uniform base plus a 32-bit lane offset.
+__device__ __forceinline__ void dma16(const unsigned char* base, uint32_t off, unsigned char* lds) {
+  __builtin_amdgcn_global_load_lds((const void*)(base + off),
+                                   (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
+}
+
 // ------------------------------------------------------------------------------------------
-// dq: 64 query columns (TQ positions x G heads, position-major) per workgroup, 16 per wave.
-template <int D>
-__global__ __launch_bounds__(kBwdWaves * 64) __attribute__((amdgpu_waves_per_eu(2)))
+// dq: 16 NW query columns (TQ positions x G heads, position-major) per workgroup, 16 per wave.
+template <int D, int NW>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2)))
 void bwd_dq_kernel(BackwardArgs a, int tq, int tiles) {
-  constexpr int NW = kBwdWaves;
   constexpr int KK = D / 32, NB = D / 16, ROWB = D * 2, PPR = D / 8, RPI = 64 / PPR;
-  constexpr int NG = 32 / RPI;
+  constexpr int NG = 32 / RPI;           // 1 KiB DMA groups per 32-row tile
   constexpr int TILE = 32 * ROWB;
-  constexpr int BUF = 2 * TILE;          // K tile (dual layout), V tile (dual layout)
+  constexpr int BUF = 2 * TILE;          // K tile, V tile (both in the dual layout)
   constexpr int STAGES = 3;
   constexpr int OPS = 2 * NG;
   constexpr int MYOPS = OPS / NW;
-  static_assert(OPS % NW == 0, "DMA split");
+  static_assert(OPS % NW == 0 && MYOPS >= 1, "DMA split");
   __shared__ __align__(16) unsigned char smem[STAGES * BUF];
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -103,7 +114,7 @@ void bwd_dq_kernel(BackwardArgs a, int tq, int tiles) {
   const int mask_lo = support_start(a.mode, a.block, a.window, t_last);
   const int mask_hi = t0;
 
-  const size_t rowstride = (size_t)a.hkv * ROWB;
+  const uint32_t rowstride = (uint32_t)a.hkv * ROWB;
   const unsigned char* kbase = (const unsigned char*)a.k + ((size_t)b * n * a.hkv + g) * ROWB;
   const unsigned char* vbase = (const unsigned char*)a.v + ((size_t)b * n * a.hkv + g) * ROWB;
 
@@ -129,48 +140,44 @@ void bwd_dq_kernel(BackwardArgs a, int tq, int tiles) {
       gB[kk] = __builtin_bit_cast(bf16x8, valid ? wg : zero);
     }
   }
-  const size_t lrow = ((size_t)b * a.hq + hc) * n + (valid ? tc : t0);
-  const float lse2 = valid ? a.lse[lrow] * 1.4426950408889634f : 0.0f;
-  const float dlt = valid ? a.delta[lrow] : 0.0f;
+  const float* wrow = a.ws + ((size_t)b * a.hq + hc) * 2 * n + (valid ? tc : t0);
+  const float lse2 = valid ? wrow[0] : 0.0f;
+  const float dlt = valid ? wrow[n] : 0.0f;
 
-  // DMA of one step (K then V rows of keys 32*(s_first+st) ..), clamped to t_last.
-  const unsigned char* src[MYOPS];
-  int row_of[MYOPS];
+  // DMA of key step st: rows k0 .. k0+31 of K then V (wave-uniform base at row k0, lane offset
+  // row * rowstride + piece); rows past t_last read the last piece of row t_last instead
+  // (masked, and inside the tensor).
+  uint32_t doff[MYOPS];
 #pragma unroll
   for (int o = 0; o < MYOPS; ++o) {
     const int op = wave * MYOPS + o;
-    const bool isv = op >= NG;
-    const int x = isv ? op - NG : op;
+    const int x = op >= NG ? op - NG : op;
     const int row = x * RPI + lane / PPR;
-    const int piece = (lane % PPR) ^ dual_swz<D>(row);
-    row_of[o] = row;
-    src[o] = (isv ? vbase : kbase) + (size_t)(s_first * 32 + row) * rowstride + piece * 16;
+    doff[o] = (uint32_t)row * rowstride + (uint32_t)(((lane % PPR) ^ dual_swz<D>(row)) * 16);
   }
-  const size_t step_bytes = 32 * rowstride;
   auto issue = [&](int stage, int st) {
     unsigned char* tp = smem + stage * BUF;
-    const bool tail = (s_first + st) * 32 + 31 > t_last;
+    const int k0 = (s_first + st) * 32;
+    const uint32_t lim = (uint32_t)min(t_last - k0, 31) * rowstride + (ROWB - 16);
 #pragma unroll
     for (int o = 0; o < MYOPS; ++o) {
       const int op = wave * MYOPS + o;
       const bool isv = op >= NG;
       const int x = isv ? op - NG : op;
-      const unsigned char* s = src[o] + (size_t)st * step_bytes;
-      if (tail) {
-        const int over = (s_first + st) * 32 + row_of[o] - t_last;
-        if (over > 0) s -= (size_t)over * rowstride;
-      }
-      __builtin_amdgcn_global_load_lds(
-          (const void*)s, (__attribute__((address_space(3))) void*)(tp + (isv ? TILE : 0) + x * 1024),
-          16, 0, 0);
+      dma16((isv ? vbase : kbase) + (size_t)k0 * rowstride, min(doff[o], lim),
+            tp + (isv ? TILE : 0) + x * 1024);
     }
   };
 
-  // Transposed-read addresses of this lane in stage 0 (K tile), chunk nb: row 4j + c/4,
-  // channels 16nb + 4(c mod 4) .. +3.
-  uint32_t kaddr[NB];
+  // LDS offsets of this lane: row-operand reads (row c16, piece 4kk + j4; row 16 + c16 and
+  // the V tile at fixed distances) and transposed reads of the K tile for chunk nb (row
+  // 4j + c/4, channels 16nb + 4(c mod 4) .. +3).
+  uint32_t roff[KK], kaddr[NB];
   {
     const uint32_t base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) unsigned char*)smem;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk)
+      roff[kk] = base + c16 * ROWB + (((4 * kk + j4) ^ dual_swz<D>(c16)) << 4);
     const int r = 4 * j4 + (c16 >> 2);
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
@@ -178,6 +185,7 @@ void bwd_dq_kernel(BackwardArgs a, int tq, int tiles) {
       kaddr[nb] = base + r * ROWB + ((p ^ dual_swz<D>(r)) << 4) + ((c16 & 1) << 3);
     }
   }
+  const __attribute__((address_space(3))) unsigned char* lds0 = nullptr;
 
   f32x4 acc[NB];
 #pragma unroll
@@ -186,6 +194,7 @@ void bwd_dq_kernel(BackwardArgs a, int tq, int tiles) {
 
   issue(0, 0);
   if (nsteps > 1) issue(1, 1);
+  int rstage = 0;
 
   auto step = [&](int st, auto masked) {
     if (st + 1 < nsteps)
@@ -193,21 +202,18 @@ void bwd_dq_kernel(BackwardArgs a, int tq, int tiles) {
     else
       __builtin_amdgcn_s_waitcnt(0x0F70);
     lds_barrier();
-    if (st + 2 < nsteps) issue((st + 2) % STAGES, st + 2);
+    if (st + 2 < nsteps) issue(rstage == 0 ? 2 : rstage - 1, st + 2);
     __builtin_amdgcn_sched_barrier(0);
-    const unsigned char* kt = smem + (st % STAGES) * BUF;
-    const unsigned char* vt = kt + TILE;
+    const uint32_t sb = (uint32_t)(rstage * BUF);
     const int k0 = (s_first + st) * 32;
     f32x4 s0 = {0.0f, 0.0f, 0.0f, 0.0f}, s1 = s0, d0 = s0, d1 = s0;
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
-      const int p = 4 * kk + j4;
-      const bf16x8 ka = *(const bf16x8*)(kt + c16 * ROWB + ((p ^ dual_swz<D>(c16)) << 4));
-      const bf16x8 kb =
-          *(const bf16x8*)(kt + (16 + c16) * ROWB + ((p ^ dual_swz<D>(16 + c16)) << 4));
-      const bf16x8 va = *(const bf16x8*)(vt + c16 * ROWB + ((p ^ dual_swz<D>(c16)) << 4));
-      const bf16x8 vb =
-          *(const bf16x8*)(vt + (16 + c16) * ROWB + ((p ^ dual_swz<D>(16 + c16)) << 4));
+      const auto* p = lds0 + roff[kk] + sb;
+      const bf16x8 ka = *(const __attribute__((address_space(3))) bf16x8*)(p);
+      const bf16x8 kb = *(const __attribute__((address_space(3))) bf16x8*)(p + 16 * ROWB);
+      const bf16x8 va = *(const __attribute__((address_space(3))) bf16x8*)(p + TILE);
+      const bf16x8 vb = *(const __attribute__((address_space(3))) bf16x8*)(p + TILE + 16 * ROWB);
       s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qB[kk], s0, 0, 0, 0);
       s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb, qB[kk], s1, 0, 0, 0);
       d0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, gB[kk], d0, 0, 0, 0);
@@ -227,7 +233,6 @@ void bwd_dq_kernel(BackwardArgs a, int tq, int tiles) {
       dsB[e] = (__bf16)(pe * (dp - dlt));
     }
     // dq^T += K^T ds^T: the K^T operand by transposed reads of the K tile.
-    const uint32_t sb = (uint32_t)((st % STAGES) * BUF);
     u32x2 kr[2 * NB];
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
@@ -251,6 +256,7 @@ void bwd_dq_kernel(BackwardArgs a, int tq, int tiles) {
       acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, w), dsB,
                                                         acc[nb], 0, 0, 0);
     }
+    rstage = rstage == STAGES - 1 ? 0 : rstage + 1;
     __builtin_amdgcn_sched_barrier(0);
   };
 
@@ -277,13 +283,13 @@ void bwd_dq_kernel(BackwardArgs a, int tq, int tiles) {
 }
 
 // ------------------------------------------------------------------------------------------
-// dk, dv: 64 keys of one KV head per workgroup (16 per wave, held as matrix-core B operands);
-// the workgroup walks (query head, 32-target step) pairs through LDS: Q and dout rows (dual
-// layout) and the steps' lse and delta values.
-template <int D>
-__global__ __launch_bounds__(kBwdWaves * 64) __attribute__((amdgpu_waves_per_eu(2)))
+// dk, dv: 16 NW keys of one KV head per workgroup (16 per wave, held as matrix-core B
+// operands); the workgroup walks, for each query head of the group in turn, the 32-target
+// steps of the targets whose supports contain its keys, through LDS: Q and dout rows (dual
+// layout) and the steps' lse * log2(e) and delta values.
+template <int D, int NW>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2)))
 void bwd_dkdv_kernel(BackwardArgs a, int tiles) {
-  constexpr int NW = kBwdWaves;
   constexpr int KK = D / 32, NB = D / 16, ROWB = D * 2, PPR = D / 8, RPI = 64 / PPR;
   constexpr int NG = 32 / RPI;
   constexpr int TILE = 32 * ROWB;
@@ -291,7 +297,7 @@ void bwd_dkdv_kernel(BackwardArgs a, int tiles) {
   constexpr int STAGES = 3;
   constexpr int ROWOPS = 2 * NG;        // row DMAs per step; wave 0 also issues the lse/delta one
   constexpr int MYOPS = ROWOPS / NW;
-  static_assert(ROWOPS % NW == 0, "DMA split");
+  static_assert(ROWOPS % NW == 0 && MYOPS >= 1, "DMA split");
   constexpr int KT = 16 * NW;           // keys per workgroup
   __shared__ __align__(16) unsigned char smem[STAGES * BUF];
 
@@ -308,10 +314,21 @@ void bwd_dkdv_kernel(BackwardArgs a, int tiles) {
   const int q_end = min(n - 1, support_last_target(a.mode, a.block, a.window, s1k));
   const int qsteps = (q_end >> 5) - (q_first >> 5) + 1;
   const int nsteps = G * qsteps;                    // (head, target step) pairs
+  // Target steps j in [ja, jb) are interior for every head: all their targets come at or after
+  // the last key and at or before the last target of the first key (the supports are
+  // intervals ending at the target, so every pair is covered); a partial key tile has none.
+  int ja = (s1k - q_first + 31) >> 5;
+  const int lim_t = min(n - 1, support_last_target(a.mode, a.block, a.window, s0k)) - 31 - q_first;
+  int jb = (lim_t < 0 || s1k - s0k + 1 != KT) ? 0 : (lim_t >> 5) + 1;
+  ja = min(ja, qsteps);
+  jb = max(ja, min(jb, qsteps));
 
   // This wave's keys as B operands: lane (key c16, slice j) holds channels 32kk + 8j .. +7.
   const int key = s0k + wave * 16 + c16;
   const bool kvalid = key < n;
+  // Targets that see this key: key .. min(q_end, last target of the key).
+  const int t_lo = kvalid ? key : 0x7fffffff;
+  const int t_hi = min(q_end, support_last_target(a.mode, a.block, a.window, key));
   bf16x8 kB[KK], vB[KK];
   {
     const size_t rowk = ((size_t)b * n + (kvalid ? key : s0k)) * a.hkv + g;
@@ -327,41 +344,50 @@ void bwd_dkdv_kernel(BackwardArgs a, int tiles) {
     }
   }
 
-  // DMA of step gs: rows of head g*G + gs / qsteps, targets q_first + 32 (gs mod qsteps) ..
-  // (clamped to q_end); wave 0 also loads the 32 lse and 32 delta values (one 4-byte DMA).
-  const size_t qrowstride = (size_t)a.hq * ROWB;
-  auto issue = [&](int stage, int gs) {
+  // DMA of (head hi, target step j): rows q0 .. q0+31 of Q and dout (wave-uniform base, lane
+  // offset row * qrowstride + piece; rows past q_end read the last piece of row q_end), and,
+  // from wave 0, lse2 (lanes 0..31) and delta (lanes 32..63) of the same targets.
+  const uint32_t qrowstride = (uint32_t)a.hq * ROWB;
+  const unsigned char* qb0 = (const unsigned char*)a.q + ((size_t)b * n * a.hq + g * G) * ROWB;
+  const unsigned char* gb0 = (const unsigned char*)a.dout + ((size_t)b * n * a.hq + g * G) * ROWB;
+  const float* wb0 = a.ws + ((size_t)b * a.hq + g * G) * 2 * n;
+  uint32_t doff[MYOPS];
+#pragma unroll
+  for (int o = 0; o < MYOPS; ++o) {
+    const int op = wave * MYOPS + o;
+    const int x = op >= NG ? op - NG : op;
+    const int row = x * RPI + lane / PPR;
+    doff[o] = (uint32_t)row * qrowstride + (uint32_t)(((lane % PPR) ^ dual_swz<D>(row)) * 16);
+  }
+  auto issue = [&](int stage, int hi, int j) {
     unsigned char* tp = smem + stage * BUF;
-    const int hi = gs / qsteps;
-    const int head = g * G + hi;
-    const int q0 = q_first + 32 * (gs - hi * qsteps);
+    const int q0 = q_first + 32 * j;
+    const int last = min(q_end - q0, 31);
+    const uint32_t lim = (uint32_t)last * qrowstride + (ROWB - 16);
+    const size_t rowbase = ((size_t)q0 * a.hq + hi) * ROWB;
 #pragma unroll
     for (int o = 0; o < MYOPS; ++o) {
       const int op = wave * MYOPS + o;
       const bool isg = op >= NG;
       const int x = isg ? op - NG : op;
-      const int row = x * RPI + lane / PPR;
-      const int t = min(q0 + row, q_end);
-      const int piece = (lane % PPR) ^ dual_swz<D>(row);
-      const unsigned char* s = (const unsigned char*)(isg ? a.dout : a.q) +
-                               ((size_t)b * n + t) * qrowstride + (size_t)head * ROWB + piece * 16;
-      __builtin_amdgcn_global_load_lds(
-          (const void*)s, (__attribute__((address_space(3))) void*)(tp + (isg ? TILE : 0) + x * 1024),
-          16, 0, 0);
+      dma16((isg ? gb0 : qb0) + rowbase, min(doff[o], lim), tp + (isg ? TILE : 0) + x * 1024);
     }
     if (wave == 0) {
-      const int t = min(q0 + (lane & 31), q_end);
-      const float* s = (lane < 32 ? a.lse : a.delta) + ((size_t)b * a.hq + head) * n + t;
+      const float* s = wb0 + (size_t)hi * 2 * n + q0 + min(lane & 31, last) + (lane >> 5) * n;
       __builtin_amdgcn_global_load_lds((const void*)s,
                                        (__attribute__((address_space(3))) void*)(tp + 2 * TILE),
                                        4, 0, 0);
     }
   };
 
-  // Transposed-read addresses (stage 0) of the Q tile for chunk nb; the dout tile is TILE on.
-  uint32_t taddr[NB];
+  // LDS offsets of this lane: row-operand reads of the Q tile (row c16, piece 4kk + j4; row
+  // 16 + c16 and the dout tile at fixed distances) and transposed reads for chunk nb.
+  uint32_t roff[KK], taddr[NB];
   {
     const uint32_t base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) unsigned char*)smem;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk)
+      roff[kk] = base + c16 * ROWB + (((4 * kk + j4) ^ dual_swz<D>(c16)) << 4);
     const int r = 4 * j4 + (c16 >> 2);
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
@@ -369,6 +395,9 @@ void bwd_dkdv_kernel(BackwardArgs a, int tiles) {
       taddr[nb] = base + r * ROWB + ((p ^ dual_swz<D>(r)) << 4) + ((c16 & 1) << 3);
     }
   }
+  const uint32_t lbase =
+      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) unsigned char*)smem + 2 * TILE;
+  const __attribute__((address_space(3))) unsigned char* lds0 = nullptr;
 
   f32x4 acck[NB], accv[NB];
 #pragma unroll
@@ -377,14 +406,24 @@ void bwd_dkdv_kernel(BackwardArgs a, int tiles) {
     accv[nb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
   }
   const float c = a.scale_log2;
-  const float log2e = 1.4426950408889634f;
 
-  issue(0, 0);
-  if (nsteps > 1) issue(1, 1);
+  // Issue cursor (head, step) two steps ahead of the step being computed.
+  int ih = 0, ij = 0;
+  auto advance = [&]() {
+    if (++ij == qsteps) {
+      ij = 0;
+      ++ih;
+    }
+  };
+  issue(0, ih, ij);
+  advance();
+  if (nsteps > 1) {
+    issue(1, ih, ij);
+    advance();
+  }
+  int rstage = 0;
 
-  // Every (target, key) of a step is in the support when all its targets come after the
-  // workgroup's last key and the first key is at or after the support start of its last target.
-  auto step = [&](int gs, auto masked) {
+  auto step = [&](int gs, int j, auto masked) {
     if (wave == 0) {
       if (gs + 1 < nsteps)
         __builtin_amdgcn_s_waitcnt(0x0F70 | ((MYOPS + 1) & 15) | (((MYOPS + 1) >> 4) << 14));
@@ -397,53 +436,49 @@ void bwd_dkdv_kernel(BackwardArgs a, int tiles) {
         __builtin_amdgcn_s_waitcnt(0x0F70);
     }
     lds_barrier();
-    if (gs + 2 < nsteps) issue((gs + 2) % STAGES, gs + 2);
+    if (gs + 2 < nsteps) {
+      issue(rstage == 0 ? 2 : rstage - 1, ih, ij);
+      advance();
+    }
     __builtin_amdgcn_sched_barrier(0);
-    const unsigned char* qt = smem + (gs % STAGES) * BUF;
-    const unsigned char* gt = qt + TILE;
-    const float* lt = (const float*)(qt + 2 * TILE);
-    const int hi = gs / qsteps;
-    const int q0 = q_first + 32 * (gs - hi * qsteps);
+    const uint32_t sb = (uint32_t)(rstage * BUF);
+    const int q0 = q_first + 32 * j;
     // Scores with targets on the rows (two halves of 16) and this wave's keys on the columns.
     f32x4 s0 = {0.0f, 0.0f, 0.0f, 0.0f}, s1 = s0, d0 = s0, d1 = s0;
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
-      const int p = 4 * kk + j4;
-      const bf16x8 qa = *(const bf16x8*)(qt + c16 * ROWB + ((p ^ dual_swz<D>(c16)) << 4));
-      const bf16x8 qb =
-          *(const bf16x8*)(qt + (16 + c16) * ROWB + ((p ^ dual_swz<D>(16 + c16)) << 4));
-      const bf16x8 ga = *(const bf16x8*)(gt + c16 * ROWB + ((p ^ dual_swz<D>(c16)) << 4));
-      const bf16x8 gb =
-          *(const bf16x8*)(gt + (16 + c16) * ROWB + ((p ^ dual_swz<D>(16 + c16)) << 4));
+      const auto* p = lds0 + roff[kk] + sb;
+      const bf16x8 qa = *(const __attribute__((address_space(3))) bf16x8*)(p);
+      const bf16x8 qb = *(const __attribute__((address_space(3))) bf16x8*)(p + 16 * ROWB);
+      const bf16x8 ga = *(const __attribute__((address_space(3))) bf16x8*)(p + TILE);
+      const bf16x8 gb = *(const __attribute__((address_space(3))) bf16x8*)(p + TILE + 16 * ROWB);
       s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa, kB[kk], s0, 0, 0, 0);
       s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qb, kB[kk], s1, 0, 0, 0);
       d0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ga, vB[kk], d0, 0, 0, 0);
       d1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gb, vB[kk], d1, 0, 0, 0);
     }
-    // lse and delta of this lane's 8 targets (rows 4j..4j+3 and 16+4j..16+4j+3).
-    const f32x4 la = *(const f32x4*)(lt + 4 * j4);
-    const f32x4 lb = *(const f32x4*)(lt + 16 + 4 * j4);
-    const f32x4 da = *(const f32x4*)(lt + 32 + 4 * j4);
-    const f32x4 db = *(const f32x4*)(lt + 48 + 4 * j4);
+    // lse2 and delta of this lane's 8 targets (rows 4j..4j+3 and 16+4j..16+4j+3).
+    const auto* lp = lds0 + lbase + sb + 16 * j4;
+    const f32x4 la = *(const __attribute__((address_space(3))) f32x4*)(lp);
+    const f32x4 lb = *(const __attribute__((address_space(3))) f32x4*)(lp + 64);
+    const f32x4 da = *(const __attribute__((address_space(3))) f32x4*)(lp + 128);
+    const f32x4 db = *(const __attribute__((address_space(3))) f32x4*)(lp + 192);
     bf16x8 pB, dsB;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const float sc = e < 4 ? s0[e] : s1[e - 4];
       const float dp = e < 4 ? d0[e] : d1[e - 4];
-      const float l2 = (e < 4 ? la[e] : lb[e - 4]) * log2e;
+      const float l2 = e < 4 ? la[e] : lb[e - 4];
       const float dl = e < 4 ? da[e] : db[e - 4];
       float pe = fast_exp2(__builtin_fmaf(sc, c, -l2));
       if constexpr (decltype(masked)::value) {
         const int t = q0 + (e < 4 ? 4 * j4 + e : 16 + 4 * j4 + (e - 4));
-        const bool in = t <= q_end && key <= t &&
-                        key >= support_start(a.mode, a.block, a.window, t);
-        pe = in ? pe : 0.0f;
+        pe = (t >= t_lo && t <= t_hi) ? pe : 0.0f;
       }
       pB[e] = (__bf16)pe;
       dsB[e] = (__bf16)(pe * (dp - dl));
     }
     // dv^T += dout^T p, dk^T += Q^T ds: dout^T and Q^T by transposed reads.
-    const uint32_t sb = (uint32_t)((gs % STAGES) * BUF);
     u32x2 qr[2 * NB], gr[2 * NB];
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
@@ -490,19 +525,15 @@ void bwd_dkdv_kernel(BackwardArgs a, int tiles) {
       acck[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, w), dsB,
                                                          acck[nb], 0, 0, 0);
     }
+    rstage = rstage == STAGES - 1 ? 0 : rstage + 1;
     __builtin_amdgcn_sched_barrier(0);
   };
 
-  // Unmasked steps: targets t in [s1k, ...] whose support starts at or before s0k.
-  for (int gs = 0; gs < nsteps; ++gs) {
-    const int hi = gs / qsteps;
-    const int q0 = q_first + 32 * (gs - hi * qsteps);
-    const int qlast = q0 + 31;
-    const bool interior = q0 >= s1k && qlast <= q_end &&
-                          support_start(a.mode, a.block, a.window, qlast) <= s0k &&
-                          s0k + KT - 1 == s1k;
-    if (interior) step(gs, std::false_type{});
-    else step(gs, std::true_type{});
+  int gs = 0;
+  for (int hi = 0; hi < G; ++hi) {
+    for (int j = 0; j < ja; ++j, ++gs) step(gs, j, std::true_type{});
+    for (int j = ja; j < jb; ++j, ++gs) step(gs, j, std::false_type{});
+    for (int j = jb; j < qsteps; ++j, ++gs) step(gs, j, std::true_type{});
   }
 
   if (kvalid) {
@@ -534,15 +565,17 @@ hipError_t launch_backward_d(const BackwardArgs& a, hipStream_t stream) {
   hipLaunchKernelGGL((bwd_delta_kernel<D>), dim3((unsigned)dblocks), dim3(256), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int tq = (16 * kBwdWaves) / a.group;
+  const int tq = (16 * kDqWaves) / a.group;
   const int qtiles = (a.n + tq - 1) / tq;
-  hipLaunchKernelGGL((bwd_dq_kernel<D>), dim3((unsigned)((size_t)a.batch * a.hkv * qtiles)),
-                     dim3(kBwdWaves * 64), 0, stream, a, tq, qtiles);
+  hipLaunchKernelGGL((bwd_dq_kernel<D, kDqWaves>),
+                     dim3((unsigned)((size_t)a.batch * a.hkv * qtiles)), dim3(kDqWaves * 64), 0,
+                     stream, a, tq, qtiles);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int ktiles = (a.n + 16 * kBwdWaves - 1) / (16 * kBwdWaves);
-  hipLaunchKernelGGL((bwd_dkdv_kernel<D>), dim3((unsigned)((size_t)a.batch * a.hkv * ktiles)),
-                     dim3(kBwdWaves * 64), 0, stream, a, ktiles);
+  const int ktiles = (a.n + 16 * kDkdvWaves - 1) / (16 * kDkdvWaves);
+  hipLaunchKernelGGL((bwd_dkdv_kernel<D, kDkdvWaves>),
+                     dim3((unsigned)((size_t)a.batch * a.hkv * ktiles)), dim3(kDkdvWaves * 64), 0,
+                     stream, a, ktiles);
   return hipGetLastError();
 }
 

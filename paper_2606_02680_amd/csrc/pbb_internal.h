@@ -66,7 +66,7 @@ struct BackwardArgs {
   void* dq;            // [batch][n][hq][d]
   void* dk;            // [batch][n][hkv][d]
   void* dv;
-  float* delta;        // workspace: dout . out per (sequence, head, position) [batch][hq][n]
+  float* ws;           // workspace [batch][hq][2][n]: lse * log2(e), then dout . out
   int32_t batch;
   int32_t n;
   int32_t hq;

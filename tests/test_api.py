@@ -238,7 +238,7 @@ def test_backward_argument_errors(fn):
         assert _backward(desc, fn, **{name: A + 8}) == 4, name
     assert _backward(desc, fn, lse=A + 2) == 4
     need = P.backward_workspace_bytes(desc, 64)
-    assert need == 2 * 8 * 64 * 4          # batch x Hq x n floats (256-byte multiple)
+    assert need == 2 * 8 * 64 * 8          # batch x Hq x n x 2 floats (256-byte multiple)
     assert _backward(desc, fn, ws=0) == 5
     assert _backward(desc, fn, ws_bytes=need - 1) == 5
     assert _backward(desc, fn, ws=A + 4, ws_bytes=need) == 4
