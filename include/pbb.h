@@ -184,7 +184,8 @@ pbb_status_t swa_decode_step_advance(const pbb_desc_t *desc, const int32_t *pos,
  *            receives k/v of the last such s; other slots are left as they are.  After
  *            pbb_ring_init and this call, decoding continues with pos[b] = n (Appendix F.1).
  * bfloat16 only (PBB_ERR_DTYPE otherwise); fp32 accumulation, output rounded RNE.  Requires
- * 0 <= n <= 2^30; n == 0 does nothing.  q, k, v, out, rings 16-byte aligned, lse 4-byte
+ * 0 <= n <= 2^30 and n_q_heads * head_dim <= 2^24 (PBB_ERR_SHAPE otherwise); n == 0 does
+ * nothing.  q, k, v, out, rings 16-byte aligned, lse 4-byte
  * aligned.  Same descriptor rules as pbb_decode_step, and rope_base must be 0 (rotate q and k
  * before the call; the ring then holds rotated keys as a rotary decode expects); no workspace.
  */

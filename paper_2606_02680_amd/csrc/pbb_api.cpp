@@ -123,6 +123,8 @@ pbb_status_t prefill_common(const pbb_desc_t* desc, bool swa, int32_t n, const v
   // Workgroups: one per (sequence, KV head, tile of at least 8 positions).
   if ((uint64_t)desc->batch * (uint64_t)desc->n_kv_heads * ((uint64_t)n / 8 + 1) > 0x7fffffffull)
     return PBB_ERR_SHAPE;
+  // 32 rows of one tensor lie within 32-bit byte offsets of the first
+  if ((uint64_t)desc->n_q_heads * (uint64_t)desc->head_dim > (1u << 24)) return PBB_ERR_SHAPE;
   if (n == 0) return PBB_OK;
 
   pbb::PrefillArgs a;

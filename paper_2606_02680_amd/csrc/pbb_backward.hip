@@ -82,12 +82,6 @@ __device__ __forceinline__ int xcd_tile() {
   return (xcd < rem ? xcd * (per + 1) : rem * (per + 1) + (xcd - rem) * per) + local;
 }
 
-// Issue of one 16-byte LDS DMA from a wave-uniform base plus a 32-bit lane offset.
-__device__ __forceinline__ void dma16(const unsigned char* base, uint32_t off, unsigned char* lds) {
-  __builtin_amdgcn_global_load_lds((const void*)(base + off),
-                                   (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
-}
-
 // ------------------------------------------------------------------------------------------
 // dq: 16 NW query columns (TQ positions x G heads, position-major) per workgroup, 16 per wave.
 template <int D, int NW>

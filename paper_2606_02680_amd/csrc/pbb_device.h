@@ -89,6 +89,14 @@ __device__ __forceinline__ float sum_xor16_32(float x) {
   return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
+// One 16-byte LDS DMA (global_load_lds) from a wave-uniform base plus a 32-bit lane offset, so
+// that the address is formed by the instruction (scalar base + vector offset) rather than by
+// 64-bit vector arithmetic.
+__device__ __forceinline__ void dma16(const unsigned char* base, uint32_t off, unsigned char* lds) {
+  __builtin_amdgcn_global_load_lds((const void*)(base + off),
+                                   (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
+}
+
 // Transposed LDS read (gfx950 ds_read_b64_tr_b16) at addr + OFF.  Issued as inline asm: the
 // compiler cannot tell these reads apart from the LDS DMA still in flight and would otherwise
 // wait for every outstanding load before each of them.  The caller waits with an s_waitcnt

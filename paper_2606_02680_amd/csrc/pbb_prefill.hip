@@ -54,7 +54,7 @@ void prefill_bf16_kernel(PrefillArgs a, int tq, int tiles) {
   constexpr int OPS = 2 * NG;           // DMA instructions per step (K tile, then V tile)
   constexpr int MYOPS = OPS / NW;       // issued by each wave
   static_assert(OPS % NW == 0, "DMA split");
-  __shared__ __align__(16) unsigned char smem[STAGES * BUF];
+  __shared__ __align__(256) unsigned char smem[STAGES * BUF];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -84,7 +84,7 @@ void prefill_bf16_kernel(PrefillArgs a, int tq, int tiles) {
   const int mask_lo = support_lo(a, t_last);
   const int mask_hi = t0;
 
-  const size_t rowstride = (size_t)a.hkv * ROWB;  // bytes between consecutive positions
+  const uint32_t rowstride = (uint32_t)a.hkv * ROWB;  // bytes between consecutive positions
   const unsigned char* kbase = (const unsigned char*)a.k + ((size_t)b * n * a.hkv + g) * ROWB;
   const unsigned char* vbase = (const unsigned char*)a.v + ((size_t)b * n * a.hkv + g) * ROWB;
 
@@ -112,25 +112,33 @@ void prefill_bf16_kernel(PrefillArgs a, int tq, int tiles) {
   }
 
   auto swz_k = [](int r) -> int { return D == 128 ? (r & 15) : ((r >> 1) & 7); };
-  // V rows are stored whole, 32-byte chunk c of row r at chunk c ^ (r mod 4), so that the
-  // transposed reads below (4 rows x 32 bytes per 16 lanes) spread over all banks.
-  auto swz_v = [](int r) -> int { return 2 * (r & 3); };  // in 16-byte pieces
-  // LDS byte addresses of this lane's transposed V reads in stage 0, for chunks nb = 0..3
-  // (chunks 4..7 of d = 128 rows sit 128 bytes further: (nb ^ q) = 4 + ((nb - 4) ^ q)).
-  uint32_t vaddr[4];
+  // V rows: 16-byte piece p of row r at p ^ swz_v(r).  The transposed reads below (4 rows x
+  // 8 bytes per 16 lanes) then hit distinct banks within every group of 32 lanes that an 8-byte
+  // LDS read serves per cycle on gfx950 (the lanes sharing the parity of lane bits 3..5).
+  auto swz_v = [](int r) -> int { return D == 128 ? 2 * (r & 7) : 2 * ((r >> 1) & 3); };
+  // LDS byte addresses of this lane's reads in stage 0: K rows c16 (and 16 + c16, a fixed
+  // distance on) at piece 4kk + j4, and the transposed V reads of chunk nb: row 4j4 + c16/4,
+  // channels 16nb + 4(c16 mod 4) .. +3 (rows 16.. a fixed distance on).  For d = 128, chunk
+  // nb + 4 sits at the byte offset of chunk nb with bit 7 flipped (rows are 256-byte aligned).
+  uint32_t kaddr[KK], vaddr[4];
   {
     const uint32_t base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) unsigned char*)smem;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk)
+      kaddr[kk] = base + c16 * ROWB + (((4 * kk + j4) ^ swz_k(c16)) << 4);
     const int vrow = 4 * j4 + (c16 >> 2);
 #pragma unroll
     for (int q = 0; q < 4; ++q)
-      vaddr[q] = base + KTILE + vrow * ROWB + ((((q ^ (c16 >> 2)) << 5) | ((c16 & 3) << 3)));
+      vaddr[q] = base + KTILE + vrow * ROWB +
+                 (((2 * q + ((c16 & 3) >> 1)) ^ swz_v(vrow)) << 4) + ((c16 & 1) << 3);
   }
+  const __attribute__((address_space(3))) unsigned char* lds0 = nullptr;
 
   // This wave's share of the DMA of a step: MYOPS 1 KiB pieces, each lane one 16-byte piece of
-  // one key row.  Row pointers start at the first step and advance 32 rows per step; in the
-  // last step, keys past t_last are clamped to t_last (read, then masked for every column).
-  const unsigned char* src[MYOPS];
-  int row_of[MYOPS];
+  // one key row, addressed as a wave-uniform base (the step's first key row) plus a 32-bit lane
+  // offset.  In the last step, rows past t_last read the last piece of row t_last instead
+  // (inside the tensor; masked for every column).
+  uint32_t doff[MYOPS];
 #pragma unroll
   for (int o = 0; o < MYOPS; ++o) {
     const int op = wave * MYOPS + o;
@@ -138,26 +146,19 @@ void prefill_bf16_kernel(PrefillArgs a, int tq, int tiles) {
     const int x = isv ? op - NG : op;
     const int row = x * RPI + lane / PPR;
     const int piece = (lane % PPR) ^ (isv ? swz_v(row) : swz_k(row));
-    row_of[o] = row;
-    src[o] = (isv ? vbase : kbase) + (size_t)(s_first * 32 + row) * rowstride + piece * 16;
+    doff[o] = (uint32_t)row * rowstride + (uint32_t)(piece * 16);
   }
-  const size_t step_bytes = 32 * rowstride;
   auto issue = [&](int stage, int st) {
     unsigned char* tile_p = smem + stage * BUF;
-    const bool tail = (s_first + st) * 32 + 31 > t_last;
+    const int k0 = (s_first + st) * 32;
+    const uint32_t lim = (uint32_t)min(t_last - k0, 31) * rowstride + (ROWB - 16);
 #pragma unroll
     for (int o = 0; o < MYOPS; ++o) {
       const int op = wave * MYOPS + o;
       const bool isv = op >= NG;
       const int x = isv ? op - NG : op;
-      const unsigned char* s = src[o] + (size_t)st * step_bytes;
-      if (tail) {
-        const int over = (s_first + st) * 32 + row_of[o] - t_last;
-        if (over > 0) s -= (size_t)over * rowstride;
-      }
-      unsigned char* dst = tile_p + (isv ? KTILE : 0) + x * 1024;
-      __builtin_amdgcn_global_load_lds((const void*)s,
-                                       (__attribute__((address_space(3))) void*)dst, 16, 0, 0);
+      dma16((isv ? vbase : kbase) + (size_t)k0 * rowstride, min(doff[o], lim),
+            tile_p + (isv ? KTILE : 0) + x * 1024);
     }
   };
 
@@ -173,6 +174,7 @@ void prefill_bf16_kernel(PrefillArgs a, int tq, int tiles) {
 
   issue(0, 0);
   if (nsteps > 1) issue(1, 1);
+  int rstage = 0;
 
   auto step = [&](int st, auto masked) {
     // This wave's loads of step st have landed once at most step st+1's are outstanding; the
@@ -183,10 +185,10 @@ void prefill_bf16_kernel(PrefillArgs a, int tq, int tiles) {
     else
       __builtin_amdgcn_s_waitcnt(0x0F70);
     lds_barrier();
-    if (st + 2 < nsteps) issue((st + 2) % STAGES, st + 2);
+    if (st + 2 < nsteps) issue(rstage == 0 ? 2 : rstage - 1, st + 2);
     __builtin_amdgcn_sched_barrier(0);
 
-    const unsigned char* tile_p = smem + (st % STAGES) * BUF;
+    const uint32_t sb = (uint32_t)(rstage * BUF);
     const int k0 = (s_first + st) * 32;
     f32x4 s0[QC], s1[QC];
 #pragma unroll
@@ -196,10 +198,9 @@ void prefill_bf16_kernel(PrefillArgs a, int tq, int tiles) {
     }
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
-      const int p = 4 * kk + j4;
-      const bf16x8 ka = *(const bf16x8*)(tile_p + c16 * ROWB + ((p ^ swz_k(c16)) << 4));
-      const bf16x8 kb =
-          *(const bf16x8*)(tile_p + (16 + c16) * ROWB + ((p ^ swz_k(16 + c16)) << 4));
+      const auto* kp = lds0 + kaddr[kk] + sb;
+      const bf16x8 ka = *(const __attribute__((address_space(3))) bf16x8*)(kp);
+      const bf16x8 kb = *(const __attribute__((address_space(3))) bf16x8*)(kp + 16 * ROWB);
 #pragma unroll
       for (int qc = 0; qc < QC; ++qc) {
         s0[qc] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qB[qc][kk], s0[qc], 0, 0, 0);
@@ -259,8 +260,7 @@ void prefill_bf16_kernel(PrefillArgs a, int tq, int tiles) {
     // 4j4..4j4+3 and 16+4j4..16+4j4+3 (the key order of P^T in the score layout).  One
     // transposed read per half: within each 16-lane group, lane i names 4 channels
     // 16nb + 4(i mod 4) .. +3 of key row 4j4 + i/4, and lane c16 receives channel 16nb + c16 of
-    // those four rows.  Chunk nb of that row sits at nb ^ (row mod 4) = nb ^ (c16 / 4).
-    const uint32_t sb = (uint32_t)((st % STAGES) * BUF);
+    // those four rows.
     u32x2 vr[2 * NB];
     constexpr int HI = 16 * ROWB;   // rows 16.. of the tile
     vr[0] = tr_read<0>(vaddr[0] + sb);
@@ -272,14 +272,14 @@ void prefill_bf16_kernel(PrefillArgs a, int tq, int tiles) {
     vr[6] = tr_read<0>(vaddr[3] + sb);
     vr[7] = tr_read<HI>(vaddr[3] + sb);
     if constexpr (NB == 8) {
-      vr[8] = tr_read<128>(vaddr[0] + sb);
-      vr[9] = tr_read<HI + 128>(vaddr[0] + sb);
-      vr[10] = tr_read<128>(vaddr[1] + sb);
-      vr[11] = tr_read<HI + 128>(vaddr[1] + sb);
-      vr[12] = tr_read<128>(vaddr[2] + sb);
-      vr[13] = tr_read<HI + 128>(vaddr[2] + sb);
-      vr[14] = tr_read<128>(vaddr[3] + sb);
-      vr[15] = tr_read<HI + 128>(vaddr[3] + sb);
+      vr[8] = tr_read<0>((vaddr[0] ^ 128u) + sb);
+      vr[9] = tr_read<HI>((vaddr[0] ^ 128u) + sb);
+      vr[10] = tr_read<0>((vaddr[1] ^ 128u) + sb);
+      vr[11] = tr_read<HI>((vaddr[1] ^ 128u) + sb);
+      vr[12] = tr_read<0>((vaddr[2] ^ 128u) + sb);
+      vr[13] = tr_read<HI>((vaddr[2] ^ 128u) + sb);
+      vr[14] = tr_read<0>((vaddr[3] ^ 128u) + sb);
+      vr[15] = tr_read<HI>((vaddr[3] ^ 128u) + sb);
       asm volatile("s_waitcnt lgkmcnt(0)"
                    : "+v"(vr[0]), "+v"(vr[1]), "+v"(vr[2]), "+v"(vr[3]), "+v"(vr[4]),
                      "+v"(vr[5]), "+v"(vr[6]), "+v"(vr[7]), "+v"(vr[8]), "+v"(vr[9]),
@@ -298,6 +298,7 @@ void prefill_bf16_kernel(PrefillArgs a, int tq, int tiles) {
       for (int qc = 0; qc < QC; ++qc)
         acc[qc][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pB[qc], acc[qc][nb], 0, 0, 0);
     }
+    rstage = rstage == STAGES - 1 ? 0 : rstage + 1;
     __builtin_amdgcn_sched_barrier(0);
   };
 
