@@ -37,8 +37,10 @@ __device__ __forceinline__ int support_lo(const PrefillArgs& a, int t) {
   return support_start(a.mode, a.block, a.window, t);
 }
 
+// Three waves per SIMD (three workgroups of 48 KiB LDS per CU): the register budget this sets
+// at d = 128 (168) leaves a few values of the epilogue in scratch, outside the key loop.
 template <int D, int QC>
-__global__ __launch_bounds__(kPrefillWaves * 64) __attribute__((amdgpu_waves_per_eu(2)))
+__global__ __launch_bounds__(kPrefillWaves * 64) __attribute__((amdgpu_waves_per_eu(3)))
 void prefill_bf16_kernel(PrefillArgs a, int tq, int tiles) {
   constexpr int NW = kPrefillWaves;
   constexpr int KK = D / 32;            // 32-channel slices of the score contraction
