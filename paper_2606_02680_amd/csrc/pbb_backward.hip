@@ -27,8 +27,10 @@
 namespace pbb {
 namespace {
 
-// Waves per workgroup of the dq and dk/dv launches (16 query columns or 16 keys per wave).
-constexpr int kDqWaves = 8;
+// Waves per workgroup of the dq and dk/dv launches (16 kDqColGroups query columns or 16 keys
+// per wave).
+constexpr int kDqWaves = 4;
+constexpr int kDqColGroups = 2;   // 16-column groups per dq wave
 constexpr int kDkdvWaves = 4;
 
 // Tiles read both as matrix-core row operands (16 bytes of one row per lane) and through
@@ -83,8 +85,9 @@ __device__ __forceinline__ int xcd_tile() {
 }
 
 // ------------------------------------------------------------------------------------------
-// dq: 16 NW query columns (TQ positions x G heads, position-major) per workgroup, 16 per wave.
-template <int D, int NW>
+// dq: 16 QC NW query columns (TQ positions x G heads, position-major) per workgroup; each wave
+// owns QC groups of 16 columns, which share every K and V read of a step.
+template <int D, int NW, int QC>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2)))
 void bwd_dq_kernel(BackwardArgs a, int tq, int tiles) {
   constexpr int KK = D / 32, NB = D / 16, ROWB = D * 2, PPR = D / 8, RPI = 64 / PPR;
@@ -116,17 +119,21 @@ void bwd_dq_kernel(BackwardArgs a, int tq, int tiles) {
   const unsigned char* kbase = (const unsigned char*)a.k + ((size_t)b * n * a.hkv + g) * ROWB;
   const unsigned char* vbase = (const unsigned char*)a.v + ((size_t)b * n * a.hkv + g) * ROWB;
 
-  // This lane's query column: position t0 + col / G, head g*G + col % G.
-  const int col = wave * 16 + c16;
-  const int cp = col / G;
-  const int tc = t0 + cp;
-  const int hc = g * G + (col - cp * G);
-  const bool valid = cp < tq && tc < n;
-  const int lo_c = valid ? support_start(a.mode, a.block, a.window, tc) : 0x7fffffff;
-  const int hi_c = valid ? tc : -1;
-  bf16x8 qB[KK], gB[KK];
-  {
-    const size_t rowq = ((size_t)b * n + (valid ? tc : t0)) * a.hq + hc;
+  // This lane's query columns: column c -> position t0 + c / G, head g*G + c % G.
+  int tc[QC], hc[QC], lo_c[QC], hi_c[QC];
+  bool valid[QC];
+  float lse2[QC], dlt[QC];
+  bf16x8 qB[QC][KK], gB[QC][KK];
+#pragma unroll
+  for (int qc = 0; qc < QC; ++qc) {
+    const int col = (wave * QC + qc) * 16 + c16;
+    const int cp = col / G;
+    tc[qc] = t0 + cp;
+    hc[qc] = g * G + (col - cp * G);
+    valid[qc] = cp < tq && tc[qc] < n;
+    lo_c[qc] = valid[qc] ? support_start(a.mode, a.block, a.window, tc[qc]) : 0x7fffffff;
+    hi_c[qc] = valid[qc] ? tc[qc] : -1;
+    const size_t rowq = ((size_t)b * n + (valid[qc] ? tc[qc] : t0)) * a.hq + hc[qc];
     const uint16_t* qrow = (const uint16_t*)a.q + rowq * D;
     const uint16_t* grow = (const uint16_t*)a.dout + rowq * D;
     const u32x4 zero = {0u, 0u, 0u, 0u};
@@ -134,13 +141,13 @@ void bwd_dq_kernel(BackwardArgs a, int tq, int tiles) {
     for (int kk = 0; kk < KK; ++kk) {
       const u32x4 wq = *(const u32x4*)(qrow + 32 * kk + 8 * j4);
       const u32x4 wg = *(const u32x4*)(grow + 32 * kk + 8 * j4);
-      qB[kk] = __builtin_bit_cast(bf16x8, valid ? wq : zero);
-      gB[kk] = __builtin_bit_cast(bf16x8, valid ? wg : zero);
+      qB[qc][kk] = __builtin_bit_cast(bf16x8, valid[qc] ? wq : zero);
+      gB[qc][kk] = __builtin_bit_cast(bf16x8, valid[qc] ? wg : zero);
     }
+    const float* wrow = a.ws + ((size_t)b * a.hq + hc[qc]) * 2 * n + (valid[qc] ? tc[qc] : t0);
+    lse2[qc] = valid[qc] ? wrow[0] : 0.0f;
+    dlt[qc] = valid[qc] ? wrow[n] : 0.0f;
   }
-  const float* wrow = a.ws + ((size_t)b * a.hq + hc) * 2 * n + (valid ? tc : t0);
-  const float lse2 = valid ? wrow[0] : 0.0f;
-  const float dlt = valid ? wrow[n] : 0.0f;
 
   // DMA of key step st: rows k0 .. k0+31 of K then V (wave-uniform base at row k0, lane offset
   // row * rowstride + piece); rows past t_last read the last piece of row t_last instead
@@ -185,9 +192,11 @@ void bwd_dq_kernel(BackwardArgs a, int tq, int tiles) {
   }
   const __attribute__((address_space(3))) unsigned char* lds0 = nullptr;
 
-  f32x4 acc[NB];
+  f32x4 acc[QC][NB];
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+  for (int qc = 0; qc < QC; ++qc)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) acc[qc][nb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
   const float c = a.scale_log2;
 
   issue(0, 0);
@@ -204,7 +213,14 @@ void bwd_dq_kernel(BackwardArgs a, int tq, int tiles) {
     __builtin_amdgcn_sched_barrier(0);
     const uint32_t sb = (uint32_t)(rstage * BUF);
     const int k0 = (s_first + st) * 32;
-    f32x4 s0 = {0.0f, 0.0f, 0.0f, 0.0f}, s1 = s0, d0 = s0, d1 = s0;
+    f32x4 s0[QC], s1[QC], d0[QC], d1[QC];
+#pragma unroll
+    for (int qc = 0; qc < QC; ++qc) {
+      s0[qc] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+      s1[qc] = s0[qc];
+      d0[qc] = s0[qc];
+      d1[qc] = s0[qc];
+    }
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
       const auto* p = lds0 + roff[kk] + sb;
@@ -212,31 +228,38 @@ void bwd_dq_kernel(BackwardArgs a, int tq, int tiles) {
       const bf16x8 kb = *(const __attribute__((address_space(3))) bf16x8*)(p + 16 * ROWB);
       const bf16x8 va = *(const __attribute__((address_space(3))) bf16x8*)(p + TILE);
       const bf16x8 vb = *(const __attribute__((address_space(3))) bf16x8*)(p + TILE + 16 * ROWB);
-      s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qB[kk], s0, 0, 0, 0);
-      s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb, qB[kk], s1, 0, 0, 0);
-      d0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, gB[kk], d0, 0, 0, 0);
-      d1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vb, gB[kk], d1, 0, 0, 0);
-    }
-    // ds = p (dp - delta), p = exp2(s c - lse2); masked keys give p = 0.
-    bf16x8 dsB;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float sc = e < 4 ? s0[e] : s1[e - 4];
-      const float dp = e < 4 ? d0[e] : d1[e - 4];
-      float pe = fast_exp2(__builtin_fmaf(sc, c, -lse2));
-      if constexpr (decltype(masked)::value) {
-        const int key = k0 + (e < 4 ? 4 * j4 + e : 16 + 4 * j4 + (e - 4));
-        pe = (key >= lo_c && key <= hi_c) ? pe : 0.0f;
+      for (int qc = 0; qc < QC; ++qc) {
+        s0[qc] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qB[qc][kk], s0[qc], 0, 0, 0);
+        s1[qc] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb, qB[qc][kk], s1[qc], 0, 0, 0);
+        d0[qc] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, gB[qc][kk], d0[qc], 0, 0, 0);
+        d1[qc] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vb, gB[qc][kk], d1[qc], 0, 0, 0);
       }
-      dsB[e] = (__bf16)(pe * (dp - dlt));
     }
-    // dq^T += K^T ds^T: the K^T operand by transposed reads of the K tile.
+    // The K^T reads for dq go out now, under the softmax arithmetic.
     u32x2 kr[2 * NB];
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
       kr[2 * nb] = tr_read<0>(kaddr[nb] + sb);
       kr[2 * nb + 1] = tr_read<16 * ROWB>(kaddr[nb] + sb);
     }
+    // ds = p (dp - delta), p = exp2(s c - lse2); masked keys give p = 0.
+    bf16x8 dsB[QC];
+#pragma unroll
+    for (int qc = 0; qc < QC; ++qc) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float sc = e < 4 ? s0[qc][e] : s1[qc][e - 4];
+        const float dp = e < 4 ? d0[qc][e] : d1[qc][e - 4];
+        float pe = fast_exp2(__builtin_fmaf(sc, c, -lse2[qc]));
+        if constexpr (decltype(masked)::value) {
+          const int key = k0 + (e < 4 ? 4 * j4 + e : 16 + 4 * j4 + (e - 4));
+          pe = (key >= lo_c[qc] && key <= hi_c[qc]) ? pe : 0.0f;
+        }
+        dsB[qc][e] = (__bf16)(pe * (dp - dlt[qc]));
+      }
+    }
+    // dq^T += K^T ds^T.
     if constexpr (NB == 8) {
       asm volatile("s_waitcnt lgkmcnt(0)"
                    : "+v"(kr[0]), "+v"(kr[1]), "+v"(kr[2]), "+v"(kr[3]), "+v"(kr[4]),
@@ -251,8 +274,10 @@ void bwd_dq_kernel(BackwardArgs a, int tq, int tiles) {
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
       const u32x4 w = {kr[2 * nb][0], kr[2 * nb][1], kr[2 * nb + 1][0], kr[2 * nb + 1][1]};
-      acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, w), dsB,
-                                                        acc[nb], 0, 0, 0);
+#pragma unroll
+      for (int qc = 0; qc < QC; ++qc)
+        acc[qc][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, w),
+                                                              dsB[qc], acc[qc][nb], 0, 0, 0);
     }
     rstage = rstage == STAGES - 1 ? 0 : rstage + 1;
     __builtin_amdgcn_sched_barrier(0);
@@ -266,15 +291,17 @@ void bwd_dq_kernel(BackwardArgs a, int tq, int tiles) {
   for (int st = st_a; st < st_b; ++st) step(st, std::false_type{});
   for (int st = st_b; st < nsteps; ++st) step(st, std::true_type{});
 
-  if (valid) {
-    uint16_t* drow = (uint16_t*)a.dq + (((size_t)b * n + tc) * a.hq + hc) * D;
+#pragma unroll
+  for (int qc = 0; qc < QC; ++qc) {
+    if (!valid[qc]) continue;
+    uint16_t* drow = (uint16_t*)a.dq + (((size_t)b * n + tc[qc]) * a.hq + hc[qc]) * D;
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
       u32x2 w;
-      w[0] = (uint32_t)float_to_bf16_rne(acc[nb][0] * a.scale) |
-             ((uint32_t)float_to_bf16_rne(acc[nb][1] * a.scale) << 16);
-      w[1] = (uint32_t)float_to_bf16_rne(acc[nb][2] * a.scale) |
-             ((uint32_t)float_to_bf16_rne(acc[nb][3] * a.scale) << 16);
+      w[0] = (uint32_t)float_to_bf16_rne(acc[qc][nb][0] * a.scale) |
+             ((uint32_t)float_to_bf16_rne(acc[qc][nb][1] * a.scale) << 16);
+      w[1] = (uint32_t)float_to_bf16_rne(acc[qc][nb][2] * a.scale) |
+             ((uint32_t)float_to_bf16_rne(acc[qc][nb][3] * a.scale) << 16);
       *(u32x2*)(drow + 16 * nb + 4 * j4) = w;
     }
   }
@@ -563,9 +590,9 @@ hipError_t launch_backward_d(const BackwardArgs& a, hipStream_t stream) {
   hipLaunchKernelGGL((bwd_delta_kernel<D>), dim3((unsigned)dblocks), dim3(256), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int tq = (16 * kDqWaves) / a.group;
+  const int tq = (16 * kDqColGroups * kDqWaves) / a.group;
   const int qtiles = (a.n + tq - 1) / tq;
-  hipLaunchKernelGGL((bwd_dq_kernel<D, kDqWaves>),
+  hipLaunchKernelGGL((bwd_dq_kernel<D, kDqWaves, kDqColGroups>),
                      dim3((unsigned)((size_t)a.batch * a.hkv * qtiles)), dim3(kDqWaves * 64), 0,
                      stream, a, tq, qtiles);
   e = hipGetLastError();
