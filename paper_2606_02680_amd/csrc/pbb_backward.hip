@@ -32,6 +32,8 @@ namespace {
 constexpr int kDqWaves = 4;
 constexpr int kDqColGroups = 2;   // 16-column groups per dq wave
 constexpr int kDkdvWaves = 4;
+constexpr int kDkdvKeyGroups = 1;  // 16-key groups per dk/dv wave
+constexpr int kDkdvWavesPerEU = 2; // occupancy the dk/dv register budget is set for
 
 // Tiles read both as matrix-core row operands (16 bytes of one row per lane) and through
 // transposed reads (4 rows x 8 bytes per 16 lanes) store 16-byte piece p of row r at p ^ g(r).
@@ -308,12 +310,13 @@ void bwd_dq_kernel(BackwardArgs a, int tq, int tiles) {
 }
 
 // ------------------------------------------------------------------------------------------
-// dk, dv: 16 NW keys of one KV head per workgroup (16 per wave, held as matrix-core B
-// operands); the workgroup walks, for each query head of the group in turn, the 32-target
-// steps of the targets whose supports contain its keys, through LDS: Q and dout rows (dual
-// layout) and the steps' lse * log2(e) and delta values.
-template <int D, int NW>
-__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2)))
+// dk, dv: 16 KC NW keys of one KV head per workgroup (KC groups of 16 per wave, held as
+// matrix-core B operands, sharing every Q and dout read of a step); the workgroup walks, for
+// each query head of the group in turn, the 32-target steps of the targets whose supports
+// contain its keys, through LDS: Q and dout rows (dual layout) and the steps' lse * log2(e)
+// and delta values.
+template <int D, int NW, int KC, int WPE>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(WPE)))
 void bwd_dkdv_kernel(BackwardArgs a, int tiles) {
   constexpr int KK = D / 32, NB = D / 16, ROWB = D * 2, PPR = D / 8, RPI = 64 / PPR;
   constexpr int NG = 32 / RPI;
@@ -323,7 +326,7 @@ void bwd_dkdv_kernel(BackwardArgs a, int tiles) {
   constexpr int ROWOPS = 2 * NG;        // row DMAs per step; wave 0 also issues the lse/delta one
   constexpr int MYOPS = ROWOPS / NW;
   static_assert(ROWOPS % NW == 0 && MYOPS >= 1, "DMA split");
-  constexpr int KT = 16 * NW;           // keys per workgroup
+  constexpr int KT = 16 * KC * NW;      // keys per workgroup
   __shared__ __align__(16) unsigned char smem[STAGES * BUF];
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -348,15 +351,18 @@ void bwd_dkdv_kernel(BackwardArgs a, int tiles) {
   ja = min(ja, qsteps);
   jb = max(ja, min(jb, qsteps));
 
-  // This wave's keys as B operands: lane (key c16, slice j) holds channels 32kk + 8j .. +7.
-  const int key = s0k + wave * 16 + c16;
-  const bool kvalid = key < n;
-  // Targets that see this key: key .. min(q_end, last target of the key).
-  const int t_lo = kvalid ? key : 0x7fffffff;
-  const int t_hi = min(q_end, support_last_target(a.mode, a.block, a.window, key));
-  bf16x8 kB[KK], vB[KK];
-  {
-    const size_t rowk = ((size_t)b * n + (kvalid ? key : s0k)) * a.hkv + g;
+  // This wave's keys as B operands: lane (key c16 of group kc, slice j) holds channels
+  // 32kk + 8j .. +7.  Targets that see a key: key .. min(q_end, last target of the key).
+  int key[KC], t_lo[KC], t_hi[KC];
+  bool kvalid[KC];
+  bf16x8 kB[KC][KK], vB[KC][KK];
+#pragma unroll
+  for (int kc = 0; kc < KC; ++kc) {
+    key[kc] = s0k + (wave * KC + kc) * 16 + c16;
+    kvalid[kc] = key[kc] < n;
+    t_lo[kc] = kvalid[kc] ? key[kc] : 0x7fffffff;
+    t_hi[kc] = min(q_end, support_last_target(a.mode, a.block, a.window, key[kc]));
+    const size_t rowk = ((size_t)b * n + (kvalid[kc] ? key[kc] : s0k)) * a.hkv + g;
     const uint16_t* krow = (const uint16_t*)a.k + rowk * D;
     const uint16_t* vrow = (const uint16_t*)a.v + rowk * D;
     const u32x4 zero = {0u, 0u, 0u, 0u};
@@ -364,8 +370,8 @@ void bwd_dkdv_kernel(BackwardArgs a, int tiles) {
     for (int kk = 0; kk < KK; ++kk) {
       const u32x4 wk = *(const u32x4*)(krow + 32 * kk + 8 * j4);
       const u32x4 wv = *(const u32x4*)(vrow + 32 * kk + 8 * j4);
-      kB[kk] = __builtin_bit_cast(bf16x8, kvalid ? wk : zero);
-      vB[kk] = __builtin_bit_cast(bf16x8, kvalid ? wv : zero);
+      kB[kc][kk] = __builtin_bit_cast(bf16x8, kvalid[kc] ? wk : zero);
+      vB[kc][kk] = __builtin_bit_cast(bf16x8, kvalid[kc] ? wv : zero);
     }
   }
 
@@ -424,12 +430,14 @@ void bwd_dkdv_kernel(BackwardArgs a, int tiles) {
       (uint32_t)(uintptr_t)(__attribute__((address_space(3))) unsigned char*)smem + 2 * TILE;
   const __attribute__((address_space(3))) unsigned char* lds0 = nullptr;
 
-  f32x4 acck[NB], accv[NB];
+  f32x4 acck[KC][NB], accv[KC][NB];
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    acck[nb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-    accv[nb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-  }
+  for (int kc = 0; kc < KC; ++kc)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      acck[kc][nb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+      accv[kc][nb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    }
   const float c = a.scale_log2;
 
   // Issue cursor (head, step) two steps ahead of the step being computed.
@@ -469,7 +477,14 @@ void bwd_dkdv_kernel(BackwardArgs a, int tiles) {
     const uint32_t sb = (uint32_t)(rstage * BUF);
     const int q0 = q_first + 32 * j;
     // Scores with targets on the rows (two halves of 16) and this wave's keys on the columns.
-    f32x4 s0 = {0.0f, 0.0f, 0.0f, 0.0f}, s1 = s0, d0 = s0, d1 = s0;
+    f32x4 s0[KC], s1[KC], d0[KC], d1[KC];
+#pragma unroll
+    for (int kc = 0; kc < KC; ++kc) {
+      s0[kc] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+      s1[kc] = s0[kc];
+      d0[kc] = s0[kc];
+      d1[kc] = s0[kc];
+    }
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
       const auto* p = lds0 + roff[kk] + sb;
@@ -477,10 +492,13 @@ void bwd_dkdv_kernel(BackwardArgs a, int tiles) {
       const bf16x8 qb = *(const __attribute__((address_space(3))) bf16x8*)(p + 16 * ROWB);
       const bf16x8 ga = *(const __attribute__((address_space(3))) bf16x8*)(p + TILE);
       const bf16x8 gb = *(const __attribute__((address_space(3))) bf16x8*)(p + TILE + 16 * ROWB);
-      s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa, kB[kk], s0, 0, 0, 0);
-      s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qb, kB[kk], s1, 0, 0, 0);
-      d0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ga, vB[kk], d0, 0, 0, 0);
-      d1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gb, vB[kk], d1, 0, 0, 0);
+#pragma unroll
+      for (int kc = 0; kc < KC; ++kc) {
+        s0[kc] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa, kB[kc][kk], s0[kc], 0, 0, 0);
+        s1[kc] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qb, kB[kc][kk], s1[kc], 0, 0, 0);
+        d0[kc] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ga, vB[kc][kk], d0[kc], 0, 0, 0);
+        d1[kc] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gb, vB[kc][kk], d1[kc], 0, 0, 0);
+      }
     }
     // lse2 and delta of this lane's 8 targets (rows 4j..4j+3 and 16+4j..16+4j+3).
     const auto* lp = lds0 + lbase + sb + 16 * j4;
@@ -488,28 +506,32 @@ void bwd_dkdv_kernel(BackwardArgs a, int tiles) {
     const f32x4 lb = *(const __attribute__((address_space(3))) f32x4*)(lp + 64);
     const f32x4 da = *(const __attribute__((address_space(3))) f32x4*)(lp + 128);
     const f32x4 db = *(const __attribute__((address_space(3))) f32x4*)(lp + 192);
-    bf16x8 pB, dsB;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float sc = e < 4 ? s0[e] : s1[e - 4];
-      const float dp = e < 4 ? d0[e] : d1[e - 4];
-      const float l2 = e < 4 ? la[e] : lb[e - 4];
-      const float dl = e < 4 ? da[e] : db[e - 4];
-      float pe = fast_exp2(__builtin_fmaf(sc, c, -l2));
-      if constexpr (decltype(masked)::value) {
-        const int t = q0 + (e < 4 ? 4 * j4 + e : 16 + 4 * j4 + (e - 4));
-        pe = (t >= t_lo && t <= t_hi) ? pe : 0.0f;
-      }
-      pB[e] = (__bf16)pe;
-      dsB[e] = (__bf16)(pe * (dp - dl));
-    }
-    // dv^T += dout^T p, dk^T += Q^T ds: dout^T and Q^T by transposed reads.
-    u32x2 qr[2 * NB], gr[2 * NB];
+    // The dout^T reads for dv go out now, under the softmax arithmetic.
+    u32x2 gr[2 * NB];
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
       gr[2 * nb] = tr_read<TILE>(taddr[nb] + sb);
       gr[2 * nb + 1] = tr_read<TILE + 16 * ROWB>(taddr[nb] + sb);
     }
+    bf16x8 pB[KC], dsB[KC];
+#pragma unroll
+    for (int kc = 0; kc < KC; ++kc) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float sc = e < 4 ? s0[kc][e] : s1[kc][e - 4];
+        const float dp = e < 4 ? d0[kc][e] : d1[kc][e - 4];
+        const float l2 = e < 4 ? la[e] : lb[e - 4];
+        const float dl = e < 4 ? da[e] : db[e - 4];
+        float pe = fast_exp2(__builtin_fmaf(sc, c, -l2));
+        if constexpr (decltype(masked)::value) {
+          const int t = q0 + (e < 4 ? 4 * j4 + e : 16 + 4 * j4 + (e - 4));
+          pe = (t >= t_lo[kc] && t <= t_hi[kc]) ? pe : 0.0f;
+        }
+        pB[kc][e] = (__bf16)pe;
+        dsB[kc][e] = (__bf16)(pe * (dp - dl));
+      }
+    }
+    // dv^T += dout^T p, dk^T += Q^T ds: dout^T and Q^T by transposed reads.
     if constexpr (NB == 8) {
       asm volatile("s_waitcnt lgkmcnt(0)"
                    : "+v"(gr[0]), "+v"(gr[1]), "+v"(gr[2]), "+v"(gr[3]), "+v"(gr[4]),
@@ -522,6 +544,7 @@ void bwd_dkdv_kernel(BackwardArgs a, int tiles) {
                      "+v"(gr[5]), "+v"(gr[6]), "+v"(gr[7]));
     }
     // The Q^T reads go out before the dv products so that they overlap them.
+    u32x2 qr[2 * NB];
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
       qr[2 * nb] = tr_read<0>(taddr[nb] + sb);
@@ -530,8 +553,10 @@ void bwd_dkdv_kernel(BackwardArgs a, int tiles) {
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
       const u32x4 w = {gr[2 * nb][0], gr[2 * nb][1], gr[2 * nb + 1][0], gr[2 * nb + 1][1]};
-      accv[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, w), pB,
-                                                         accv[nb], 0, 0, 0);
+#pragma unroll
+      for (int kc = 0; kc < KC; ++kc)
+        accv[kc][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, w),
+                                                               pB[kc], accv[kc][nb], 0, 0, 0);
     }
     if constexpr (NB == 8) {
       asm volatile("s_waitcnt lgkmcnt(0)"
@@ -547,8 +572,10 @@ void bwd_dkdv_kernel(BackwardArgs a, int tiles) {
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
       const u32x4 w = {qr[2 * nb][0], qr[2 * nb][1], qr[2 * nb + 1][0], qr[2 * nb + 1][1]};
-      acck[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, w), dsB,
-                                                         acck[nb], 0, 0, 0);
+#pragma unroll
+      for (int kc = 0; kc < KC; ++kc)
+        acck[kc][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, w),
+                                                               dsB[kc], acck[kc][nb], 0, 0, 0);
     }
     rstage = rstage == STAGES - 1 ? 0 : rstage + 1;
     __builtin_amdgcn_sched_barrier(0);
@@ -561,21 +588,23 @@ void bwd_dkdv_kernel(BackwardArgs a, int tiles) {
     for (int j = jb; j < qsteps; ++j, ++gs) step(gs, j, std::true_type{});
   }
 
-  if (kvalid) {
-    const size_t rowk = ((size_t)b * n + key) * a.hkv + g;
+#pragma unroll
+  for (int kc = 0; kc < KC; ++kc) {
+    if (!kvalid[kc]) continue;
+    const size_t rowk = ((size_t)b * n + key[kc]) * a.hkv + g;
     uint16_t* dkrow = (uint16_t*)a.dk + rowk * D;
     uint16_t* dvrow = (uint16_t*)a.dv + rowk * D;
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
       u32x2 wk, wv;
-      wk[0] = (uint32_t)float_to_bf16_rne(acck[nb][0] * a.scale) |
-              ((uint32_t)float_to_bf16_rne(acck[nb][1] * a.scale) << 16);
-      wk[1] = (uint32_t)float_to_bf16_rne(acck[nb][2] * a.scale) |
-              ((uint32_t)float_to_bf16_rne(acck[nb][3] * a.scale) << 16);
-      wv[0] = (uint32_t)float_to_bf16_rne(accv[nb][0]) |
-              ((uint32_t)float_to_bf16_rne(accv[nb][1]) << 16);
-      wv[1] = (uint32_t)float_to_bf16_rne(accv[nb][2]) |
-              ((uint32_t)float_to_bf16_rne(accv[nb][3]) << 16);
+      wk[0] = (uint32_t)float_to_bf16_rne(acck[kc][nb][0] * a.scale) |
+              ((uint32_t)float_to_bf16_rne(acck[kc][nb][1] * a.scale) << 16);
+      wk[1] = (uint32_t)float_to_bf16_rne(acck[kc][nb][2] * a.scale) |
+              ((uint32_t)float_to_bf16_rne(acck[kc][nb][3] * a.scale) << 16);
+      wv[0] = (uint32_t)float_to_bf16_rne(accv[kc][nb][0]) |
+              ((uint32_t)float_to_bf16_rne(accv[kc][nb][1]) << 16);
+      wv[1] = (uint32_t)float_to_bf16_rne(accv[kc][nb][2]) |
+              ((uint32_t)float_to_bf16_rne(accv[kc][nb][3]) << 16);
       *(u32x2*)(dkrow + 16 * nb + 4 * j4) = wk;
       *(u32x2*)(dvrow + 16 * nb + 4 * j4) = wv;
     }
@@ -597,8 +626,9 @@ hipError_t launch_backward_d(const BackwardArgs& a, hipStream_t stream) {
                      stream, a, tq, qtiles);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int ktiles = (a.n + 16 * kDkdvWaves - 1) / (16 * kDkdvWaves);
-  hipLaunchKernelGGL((bwd_dkdv_kernel<D, kDkdvWaves>),
+  constexpr int KT = 16 * kDkdvKeyGroups * kDkdvWaves;
+  const int ktiles = (a.n + KT - 1) / KT;
+  hipLaunchKernelGGL((bwd_dkdv_kernel<D, kDkdvWaves, kDkdvKeyGroups, kDkdvWavesPerEU>),
                      dim3((unsigned)((size_t)a.batch * a.hkv * ktiles)), dim3(kDkdvWaves * 64), 0,
                      stream, a, ktiles);
   return hipGetLastError();
