@@ -327,15 +327,17 @@ def paper_latency(device, shapes=(10, 12, 14), origins=(8192,), steps=256, reps=
     return res
 
 
-def cpu_baseline(cfg, t0, device, budget_s=12.0):
-    """Time the fp64 CPU oracle on the first decode step of the workload's first sequences,
-    repeating the sample until ``budget_s`` seconds have elapsed."""
+def cpu_baseline(cfg, t0, device, budget_s=12.0, n_seq=32, min_reps=1, threads=None):
+    """Time the fp64 CPU oracle on the first decode step of the workload's first ``n_seq``
+    sequences, repeating the sample at least ``min_reps`` times and until ``budget_s`` seconds
+    have elapsed."""
     import numpy as np
     import torch
     import oracle
     import workloads as W
-    threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or (os.cpu_count() or 1)
-    n = min(32, cfg.batch)
+    if threads is None:
+        threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or (os.cpu_count() or 1)
+    n = min(n_seq, cfg.batch)
     rows = torch.arange(n, dtype=torch.int64)
     back = cfg.slots
     lo = t0[:n] - back
@@ -352,7 +354,7 @@ def cpu_baseline(cfg, t0, device, budget_s=12.0):
         oracle.decode(mode, pos, q, kh, vh, lo.numpy(), block=cfg.block, window=cfg.window,
                       n_threads=threads)
         done += n
-        if time.perf_counter() - w0 >= budget_s:
+        if done >= min_reps * n and time.perf_counter() - w0 >= budget_s:
             break
     el = time.perf_counter() - w0
     model = ""
@@ -365,6 +367,42 @@ def cpu_baseline(cfg, t0, device, budget_s=12.0):
             "sample": f"first decode step of sequences 0..{n - 1} of {cfg.name} (all {cfg.hq} "
                       f"query heads each), repeated {done // n}x over {el:.1f} s; fp64 C oracle, "
                       f"{threads} threads; host CPU: {model}"}
+
+
+def copy_ceiling(device, reps=5):
+    """HBM rate of a plain 1 GiB device-to-device copy (bytes read + written per second, HIP
+    events on the copy's stream): the measured ceiling the decode rate is also compared with."""
+    import torch
+    n = 1 << 29  # 1 GiB of bf16
+    x = torch.ones(n, dtype=torch.bfloat16, device=device)
+    y = torch.empty_like(x)
+    y.copy_(x)
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        y.copy_(x)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    gbps = 4.0 * n * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del x, y
+    torch.cuda.empty_cache()
+    return gbps
+
+
+def oracle_timing(device):
+    """The fp64 CPU oracle on full batches: the first decode step of every sequence of c3, c4
+    and c5, three times each with all host threads, and once single-threaded (c3)."""
+    import workloads as W
+    res = {"host_threads": os.cpu_count()}
+    for name in ("c3", "c4", "c5"):
+        cfg = W.get_config(name)
+        t0 = W.initial_positions(cfg)
+        res[name] = cpu_baseline(cfg, t0, device, budget_s=0.0, n_seq=cfg.batch, min_reps=3)
+    cfg = W.get_config("c3")
+    res["c3_single_thread"] = cpu_baseline(cfg, W.initial_positions(cfg), device, budget_s=0.0,
+                                           n_seq=cfg.batch, min_reps=1, threads=1)
+    return res
 
 
 def main(argv=None):
@@ -382,6 +420,8 @@ def main(argv=None):
                     help="only run the prefill measurements (c3 head shapes and paper shape)")
     ap.add_argument("--backward", action="store_true",
                     help="only run the training-backward measurements (same shapes as prefill)")
+    ap.add_argument("--oracle-timing", action="store_true",
+                    help="only time the CPU oracle on full batches of c3, c4, c5 (minutes)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only time a plain 1 GiB device copy (HBM counter calibration)")
     args = ap.parse_args(argv)
@@ -416,6 +456,10 @@ def main(argv=None):
 
     if args.prefill:
         print(json.dumps({"prefill": prefill_extras(device)}), flush=True)
+        return 0
+
+    if args.oracle_timing:
+        print(json.dumps({"oracle_timing": oracle_timing(device)}), flush=True)
         return 0
 
     if args.backward:
@@ -508,6 +552,9 @@ def main(argv=None):
             device, shapes=(10, 12, 14), origins=(8192, 1048576))
         extra["prefill"] = prefill_extras(device)
         extra["backward"] = backward_extras(device)
+        copy_gbps = copy_ceiling(device)
+        extra["hbm_copy_ceiling"] = {"copy_gbps_read_plus_write": copy_gbps,
+                                     "graded_kernel_frac_of_copy": achieved / copy_gbps}
         result["extra"] = extra
         result["paper_context"] = ("Flash-PBB 1.82x Flash-SWA decode-core throughput on an RTX "
                                    "4090 (48 GB), BF16, batch 1, Hkv 2, d 64, b 128 vs w 128")
