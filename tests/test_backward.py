@@ -95,3 +95,55 @@ def test_backward_is_deterministic(cuda):
     b, _ = _run("pbb", 1, 260, 12, 2, 64, 128, 0, cuda)
     for x, y in zip(a, b):
         assert np.array_equal(x.view(np.uint32), y.view(np.uint32))
+
+
+@pytest.mark.parametrize("name,shape", __import__("bench").BACKWARD_SHAPES,
+                         ids=[nm for nm, _ in __import__("bench").BACKWARD_SHAPES])
+def test_backward_bench_shapes(cuda, name, shape):
+    """The bench's backward launches at full size.  The upstream gradient is nonzero only on a
+    prefix [0, npre) and on the targets t >= t1 = lo + span of a tail window [lo, n) (lo a
+    multiple of B for PBB, so those targets keep their full-prompt supports): the gradients there
+    match the oracle on the prefix and on the tail sub-prompt, for two (sequence, KV-head group)
+    slices, and every other gradient row is exactly zero."""
+    from tests.test_prefill import _window_plan
+    mode = "pbb" if shape.get("block") else "swa"
+    block, window = shape.get("block", 0), shape.get("window", 0)
+    batch, n, hq, hkv, d = shape["batch"], shape["n"], shape["hq"], shape["hkv"], shape["d"]
+    G = hq // hkv
+    cfg = W.Config(f"bwd-bench-{name}", mode, batch=batch, hq=hq, hkv=hkv, d=d, block=block,
+                   slots=block or window, window=window, dtype="bf16", seed=7, value_scale=1.0,
+                   pos_hi=0, steps=1)
+    q, k, v = W.prompt(cfg, n, device=cuda)
+    dfull, _, _ = W.prompt(cfg.with_(seed=8), n, device=cuda)
+    npre, lo, t1 = _window_plan(n, block or window, mode)
+    keep = torch.zeros(n, dtype=dfull.dtype, device=cuda)
+    keep[:npre] = 1
+    keep[t1:] = 1
+    dout = (dfull * keep.view(1, n, 1, 1)).contiguous()
+    if mode == "pbb":
+        desc = P.make_desc(batch, hq, hkv, d, block=block, dtype=torch.bfloat16)
+        fwd, bwd = P.pbb_prefill, P.pbb_backward
+    else:
+        desc = P.make_desc(batch, hq, hkv, d, window=window, slots=window, dtype=torch.bfloat16)
+        fwd, bwd = P.swa_prefill, P.swa_backward
+    out = torch.empty_like(q)
+    lse = torch.empty((batch, hq, n), dtype=torch.float32, device=cuda)
+    fwd(desc, q, k, v, out, lse)
+    dq, dk, dv = (torch.full_like(x, float("nan")) for x in (q, k, v))
+    print(f"[backward] {name} npre={npre} lo={lo} t1={t1}", flush=True)
+    bwd(desc, q, k, v, out, dout, lse, dq, dk, dv)
+    torch.cuda.synchronize()
+    # rows no nonzero upstream gradient reaches are exactly zero
+    assert not dq[:, npre:t1].any().item() and not dk[:, npre:lo].any().item()
+    assert not dv[:, npre:lo].any().item()
+    om = oracle.SWA if mode == "swa" else oracle.PBB
+    for b, g in ((0, 0), (batch - 1, hkv - 1)):
+        hs = slice(g * G, (g + 1) * G)
+        for a0, a1 in ((0, npre), (lo, n)):
+            sl = lambda x, h: to_np(x[b:b + 1, a0:a1, h])
+            rq, rk, rv = oracle.backward(om, sl(q, hs), sl(k, slice(g, g + 1)),
+                                         sl(v, slice(g, g + 1)), sl(dout, hs), block=block,
+                                         window=window)
+            _grad_ok(f"{name} dq seq {b} group {g} [{a0}, {a1})", sl(dq, hs), rq)
+            _grad_ok(f"{name} dk seq {b} group {g} [{a0}, {a1})", sl(dk, slice(g, g + 1)), rk)
+            _grad_ok(f"{name} dv seq {b} group {g} [{a0}, {a1})", sl(dv, slice(g, g + 1)), rv)

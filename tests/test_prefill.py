@@ -138,3 +138,40 @@ def test_prefill_is_deterministic_and_leaves_inputs(cuda):
     assert torch.equal(o1.view(torch.int16), o2.view(torch.int16))
     for x, c in zip((q, k, v), copies):
         assert torch.equal(x.view(torch.int16), c.view(torch.int16))
+
+
+def _window_plan(n, span, mode, tail=512, npre=1024):
+    """Prefix [0, npre) and a tail sub-prompt [lo, n) whose targets t >= t1 = lo + span have the
+    same support as in the full prompt (lo a multiple of B for PBB: the supports are
+    shift-invariant by whole blocks once the max(0, .) of a(t) is inactive)."""
+    npre = min(npre, n)
+    lo = n - span - tail
+    if mode == "pbb":
+        lo = (lo // span) * span
+    return npre, max(lo, npre), max(lo, npre) + span
+
+
+@pytest.mark.parametrize("name,shape", __import__("bench").PREFILL_SHAPES,
+                         ids=[nm for nm, _ in __import__("bench").PREFILL_SHAPES])
+def test_prefill_bench_shapes(cuda, name, shape):
+    """The bench's prefill launches at full size (its grid, tiles and head shapes): a prefix and
+    a block-aligned tail window of two (sequence, KV-head group) slices against the oracle."""
+    mode = "pbb" if shape.get("block") else "swa"
+    block, window = shape.get("block", 0), shape.get("window", 0)
+    cfg = _cfg(mode, shape["batch"], shape["n"], shape["hq"], shape["hkv"], shape["d"],
+               block=block, window=window, seed=7)
+    n, G = shape["n"], shape["hq"] // shape["hkv"]
+    desc, (q, k, v), out, lse, _, _ = _run(cfg, n, cuda, rings=False)
+    npre, lo, t1 = _window_plan(n, block or window, mode)
+    m = oracle.SWA if mode == "swa" else oracle.PBB
+    for b, g in ((0, 0), (shape["batch"] - 1, shape["hkv"] - 1)):
+        hs = slice(g * G, (g + 1) * G)
+        for a0, a1, first in ((0, npre, 0), (lo, n, t1 - lo)):
+            qs = to_np(q[b:b + 1, a0:a1, hs])
+            ks = to_np(k[b:b + 1, a0:a1, g:g + 1])
+            vs = to_np(v[b:b + 1, a0:a1, g:g + 1])
+            ref, ref_lse = oracle.prefill(m, qs, ks, vs, block=block, window=window)
+            got = to_np(out[b:b + 1, a0 + first:a1, hs])
+            compare(cfg, got, ref[:, first:], what=f"{name} seq {b} group {g} [{a0 + first}, {a1})")
+            gl = lse[b:b + 1, hs, a0 + first:a1].cpu().numpy().astype(np.float64)
+            assert np.abs(gl - ref_lse[:, :, first:]).max() <= 2e-3
