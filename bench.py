@@ -199,9 +199,26 @@ def prefill_measure(device, batch, n, hq, hkv, d, block=0, window=0, reps=10):
     torch.cuda.synchronize()
     ms = sorted(e0.elapsed_time(e1) for e0, e1 in ev)[reps // 2]
     flops = 4.0 * d * hq * batch * prefill_support_total(n, block, window)
+    # q, k, v read, out written (bf16), lse written (fp32), the ring's last `slots` rows written
+    nbytes = (batch * n * (2 * hq + 2 * hkv) * d * 2 + batch * hq * n * 4
+              + 2 * batch * hkv * min(n, block or window) * d * 2)
+    return _rates(ms, flops, nbytes, batch * n)
+
+
+def _rates(ms, flops, nbytes, tokens):
+    """Rates of one launch (or call) against both ceilings; `bound` names the one whose floor
+    time (algorithmic FLOPs at the bf16 matrix-core peak, or algorithmic bytes at 8 TB/s) is
+    longer, and `frac_of_bound` is that floor over the measured time."""
     tflops = flops / (ms * 1e-3) / 1e12
+    gbps = nbytes / (ms * 1e-3) / 1e9
+    t_mfma = flops / (MFMA_BF16_PEAK_TFLOPS * 1e12)
+    t_hbm = nbytes / (HBM_PEAK_GBPS * 1e9)
+    bound = "mfma" if t_mfma >= t_hbm else "hbm"
     return {"kernel_ms": ms, "tflops": tflops, "frac_of_bf16_mfma_peak": tflops / MFMA_BF16_PEAK_TFLOPS,
-            "tokens_per_s": batch * n / (ms * 1e-3), "algorithmic_tflop": flops / 1e12}
+            "hbm_gbps": gbps, "frac_of_hbm_peak": gbps / HBM_PEAK_GBPS, "bound": bound,
+            "frac_of_bound": max(t_mfma, t_hbm) / (ms * 1e-3),
+            "tokens_per_s": tokens / (ms * 1e-3), "algorithmic_tflop": flops / 1e12,
+            "algorithmic_gb": nbytes / 1e9}
 
 
 def prefill_extras(device):
@@ -249,9 +266,9 @@ def backward_measure(device, batch, n, hq, hkv, d, block=0, window=0, reps=10):
     torch.cuda.synchronize()
     ms = sorted(e0.elapsed_time(e1) for e0, e1 in ev)[reps // 2]
     flops = 10.0 * d * hq * batch * prefill_support_total(n, block, window)
-    tflops = flops / (ms * 1e-3) / 1e12
-    return {"ms": ms, "tflops": tflops, "frac_of_bf16_mfma_peak": tflops / MFMA_BF16_PEAK_TFLOPS,
-            "tokens_per_s": batch * n / (ms * 1e-3), "algorithmic_tflop": flops / 1e12}
+    # q, k, v, out, dout read and dq, dk, dv written (bf16), lse read (fp32)
+    nbytes = batch * n * (4 * hq + 4 * hkv) * d * 2 + batch * hq * n * 4
+    return _rates(ms, flops, nbytes, batch * n)
 
 
 BACKWARD_SHAPES = tuple((name.replace("prefill", "backward"), shape)

@@ -29,9 +29,11 @@
 namespace pbb {
 namespace {
 
-constexpr int kPrefillWaves = 4;
-constexpr int kPrefillColGroups = 2;   // 16-column groups per wave
-constexpr int kPrefillCols = 16 * kPrefillColGroups * kPrefillWaves;
+// Waves per workgroup and 16-column groups per wave (d = 128, d = 64).
+constexpr int kPrefillWaves128 = 4;
+constexpr int kPrefillWaves64 = 4;
+constexpr int kPrefillColGroups128 = 2;
+constexpr int kPrefillColGroups64 = 2;
 
 __device__ __forceinline__ int support_lo(const PrefillArgs& a, int t) {
   return support_start(a.mode, a.block, a.window, t);
@@ -39,10 +41,9 @@ __device__ __forceinline__ int support_lo(const PrefillArgs& a, int t) {
 
 // Three waves per SIMD (three workgroups of 48 KiB LDS per CU): the register budget this sets
 // at d = 128 (168) leaves a few values of the epilogue in scratch, outside the key loop.
-template <int D, int QC>
-__global__ __launch_bounds__(kPrefillWaves * 64) __attribute__((amdgpu_waves_per_eu(3)))
+template <int D, int QC, int NW>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(3)))
 void prefill_bf16_kernel(PrefillArgs a, int tq, int tiles) {
-  constexpr int NW = kPrefillWaves;
   constexpr int KK = D / 32;            // 32-channel slices of the score contraction
   constexpr int NB = D / 16;            // 16-channel blocks of the output
   constexpr int ROWB = D * 2;           // bytes of one K or V row
@@ -355,13 +356,15 @@ void prefill_bf16_kernel(PrefillArgs a, int tq, int tiles) {
 
 template <int D>
 hipError_t launch_prefill_d(const PrefillArgs& a, hipStream_t stream) {
-  const int tq = kPrefillCols / a.group;
+  constexpr int QC = D == 128 ? kPrefillColGroups128 : kPrefillColGroups64;
+  constexpr int NW = D == 128 ? kPrefillWaves128 : kPrefillWaves64;
+  const int tq = 16 * QC * NW / a.group;
   const int tiles = (a.n + tq - 1) / tq;
   const size_t blocks = (size_t)a.batch * a.hkv * tiles;
   if (blocks == 0) return hipSuccess;
   if (blocks > 0x7fffffffull) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((prefill_bf16_kernel<D, kPrefillColGroups>), dim3((unsigned)blocks),
-                     dim3(kPrefillWaves * 64), 0, stream, a, tq, tiles);
+  hipLaunchKernelGGL((prefill_bf16_kernel<D, QC, NW>), dim3((unsigned)blocks),
+                     dim3(NW * 64), 0, stream, a, tq, tiles);
   return hipGetLastError();
 }
 
