@@ -8,9 +8,11 @@
 //   ds_s  = p_s (g_t.v_s - delta_t),   delta_t = g_t.o_t
 //   dq_t  = scale sum_s ds_s k_s,      dk_s += scale ds_s q_t
 // summed over the query heads of each KV head for dk and dv.  Three launches:
-//   delta: one fp32 dot product per (sequence, head, position) into the workspace;
-//   dq:    the prefill kernel's structure (64 query columns per workgroup walk their key
-//          interval in 32-key steps through LDS), no running maximum (lse is known);
+//   delta: lse * log2(e) and one fp32 dot product per (sequence, head, position) into the
+//          workspace;
+//   dq:    the prefill kernel's structure (128 query columns per workgroup, two 16-column
+//          groups per wave, walk their key interval in 32-key steps through LDS), no running
+//          maximum (lse is known);
 //   dk/dv: transposed roles: each workgroup holds 64 keys of one KV head in registers and
 //          walks, for every query head of the group, the interval of targets whose supports
 //          contain those keys (PBB: up to h(floor(s/h) + 2) - 1; SWA: s + W - 1).
