@@ -18,6 +18,7 @@
 // log2(e), with a running maximum (online softmax) and fp32 accumulation (Eq.(attention)).
 
 #include <hip/hip_runtime.h>
+#include <type_traits>
 #include <stdint.h>
 
 #include "pbb_device.h"
@@ -261,29 +262,37 @@ __global__ __launch_bounds__(256) void decode_f32_kernel(DecodeArgs a) {
 //           operand (lane l: key l%16, channels 32kk + 8(l/16) .. +7) is one 16-byte LDS read,
 //           the B operand holds the group's queries, padded to 16 heads with zeros.
 //   softmax lane (head h = l%16, quarter j = l/16) holds the scores of keys 4j..4j+3 and
-//           16+4j..16+4j+3; the running maximum is shared across the four quarters.
+//           16+4j..16+4j+3; the column maximum is shared across the four quarters with
+//           permlane swaps.  The reference maximum moves (and the accumulators are rescaled)
+//           only when some head's maximum exceeds it by more than 8 in log2 units, decided
+//           wave-uniformly, so most steps skip the rescale; weights stay <= 2^8 and numerator
+//           and denominator share every reference (the same softmax).
 //   values  O^T[16 channels][16 heads] += V^T P^T.  P^T's B operand is exactly the score
-//           registers (rounded to bf16), so the key order of the contraction is fixed by the
-//           score layout; V is read back from LDS transposed, one bf16 per lane and row.
-// K and V rows travel from HBM straight into wave-private LDS tiles (global_load_lds_dwordx4
-// with the non-temporal hint: the ring is read once per step), two steps deep: while step s
+//           registers (rounded to bf16); V^T comes from transposed LDS reads
+//           (ds_read_b64_tr_b16: lane i of each 16-lane group names 4 channels of key row
+//           4j + i/4, lane c receives channel c of those four rows).
+// K and V rows travel from HBM straight into wave-private LDS tiles (global_load_lds_dwordx4,
+// with the non-temporal hint when the rings exceed the caches), two steps deep: while step s
 // computes, the loads of step s + NW are in flight, and step s + 2NW is issued right after.
-// No loaded value lands in a register, so the only memory wait is the explicit
-// vmcnt(OPS) at the top of a step: loads retire in issue order and exactly OPS loads (the
-// next step's) are issued after the current step's.  Steps past the end are still issued,
-// with every key reading the current token's cached row, to keep that count fixed.  Padded
-// heads (h >= G) compute on zero queries and are never stored.  Wave results are merged
-// through LDS with Eq.(lse) (Appendix A.4) and written as bf16 (RNE).
+// A step's loads address the ring from a wave-uniform base: inside one slot range, row r of
+// the step sits at a fixed per-lane offset from the range's first row; only steps that cross a
+// range boundary, the current token or the end compute slots per lane.  The current token's row
+// is not read from the ring: its K and V rows are loaded into registers at launch, and the wave
+// that owns its step writes them into its LDS tiles (the DMA of that row reads slot 0, which is
+// then overwritten).  No loaded value other than these lands in a register, so the only memory
+// waits are the explicit vmcnt(OPS) at the top of a step: loads retire in issue order and
+// exactly OPS loads (the next step's) are issued after the current step's.  Steps past the
+// end are still issued (reading slot 0) to keep that count fixed.  Padded heads (h >= G)
+// compute on zero queries and are never stored.  Wave results are merged through LDS with
+// Eq.(lse) (Appendix A.4) and written as bf16 (RNE).
 //
-// Tile layouts.  One 16-byte DMA of the wave writes 1 KiB: lane l lands at byte 16 l, i.e.
-// RPI whole rows.  K rows are contiguous; the 16-byte piece p of row r sits at piece slot
-// p ^ kswz(r), which spreads the 16 rows read by one MFMA operand over all banks.  V groups of
-// RPI rows are padded (and, for D = 64, the upper row quad is piece-swizzled) so that the
-// transposed reads of rows 4j+e (j = 0..3) hit 32 distinct banks.
+// Tile layout.  One 16-byte DMA of the wave writes 1 KiB: lane l lands at byte 16 l, i.e. RPI
+// whole rows.  Piece p of row r sits at piece slot p ^ swz(r), with swz(r) = 2 (r mod 8) for
+// 256-byte rows and 2 ((r >> 1) mod 4) for 128-byte rows: both the 16-byte row reads of the
+// scores and the transposed reads of the values hit distinct banks within every group of lanes
+// that gfx950 serves per cycle.
 template <int D, int NW, bool NT, bool ROPE>
 __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
-  // NT: stream the ring with the non-temporal hint (rings far larger than the caches); without
-  // it, small rings that are re-read every step can stay cache-resident.
   constexpr int kPolicy = NT ? kCachePolicyNT : 0;
   constexpr int KK = D / 32;            // 32-channel slices of the score contraction
   constexpr int NB = D / 16;            // 16-channel blocks of the output
@@ -291,10 +300,8 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
   constexpr int PPR = D / 8;            // 16-byte pieces per row
   constexpr int RPI = 64 / PPR;         // rows per 1 KiB DMA group
   constexpr int NG = 32 / RPI;          // DMA groups per step and tensor
-  constexpr int VPITCH = 1024 + (D == 128 ? 32 : 64);
-  constexpr int KTILE = 32 * ROWB;
-  constexpr int VTILE = NG * VPITCH;
-  constexpr int BUF = KTILE + VTILE;    // one step: K tile then V tile
+  constexpr int TILE = 32 * ROWB;
+  constexpr int BUF = 2 * TILE;         // one step: K tile then V tile
   constexpr int OPS = 2 * NG;           // DMA instructions per step
   constexpr int QTILE = 16 * ROWB;      // the group's queries, 16 rows (heads >= G unused)
   constexpr int STAGE_BYTES = NW * (2 * BUF + QTILE);
@@ -326,12 +333,14 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
   const uint16_t* vnew = (const uint16_t*)a.v_new + (size_t)bg * D;
   if (a.pos_next != nullptr && g == 0 && tid == 0) a.pos_next[b] = t + 1;
 
-  // The current token's row for the append: loaded now, stored at the end, so that only the
-  // store sits on the tail of a latency-bound launch.
-  const bool appender = wave == 0 && lane < 2 * PPR;
-  u32x4 append_row = {0u, 0u, 0u, 0u};
-  if (appender)
-    append_row = *(const u32x4*)((lane < PPR ? knew : vnew) + (lane % PPR) * 8);
+  auto swz = [](int r) -> int { return D == 128 ? 2 * (r & 7) : 2 * ((r >> 1) & 3); };
+
+  // The current token's K and V rows (lanes < PPR: K piece l, lanes PPR..2PPR-1: V piece l-PPR),
+  // in every wave: the wave that owns the token's step writes them into its tiles, and wave 0
+  // stores them into the ring at the end.
+  const bool rowlane = lane < 2 * PPR;
+  u32x4 cur_row = {0u, 0u, 0u, 0u};
+  if (rowlane) cur_row = *(const u32x4*)((lane < PPR ? knew : vnew) + (lane % PPR) * 8);
 
   bf16x8 qB[KK];
   float m = kNegInf;
@@ -340,7 +349,7 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 
-  unsigned char* buf[2] = {smem + (wave * 2) * BUF, smem + (wave * 2 + 1) * BUF};
+  unsigned char* const wbuf = smem + wave * 2 * BUF;   // this wave's two step buffers
   unsigned char* qtile = smem + NW * 2 * BUF + wave * QTILE;
   const int nsteps = (n_total + 31) >> 5;
 
@@ -382,113 +391,166 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
     }
   }
 
-  // Row offset (elements) of key i in its ring, or of the current token's row.
-  auto row_of = [&](int i, const uint16_t* ring, const uint16_t* fresh) -> const uint16_t* {
-    return i < R.n_ring ? ring + (size_t)ring_slot(R, i) * D : fresh;
-  };
-  auto kswz = [](int r) -> int { return D == 128 ? (r & 15) : ((r >> 1) & 7); };
-  auto vswz = [](int rr) -> int { return (D == 64 && rr >= 4) ? 2 : 0; };
-
+  // DMA of one step.  Lane l loads 16-byte piece (l mod PPR) ^ swz(row) of rows
+  // row = x RPI + l / PPR, x < NG, into LDS byte x 1024 + 16 l of the K tile and of the V tile.
+  const unsigned char* const kring_b = (const unsigned char*)kring;
+  const unsigned char* const vring_b = (const unsigned char*)vring;
+  uint32_t rowoff[NG];   // offset of this lane's piece of row x RPI + l / PPR from row 0
+#pragma unroll
+  for (int x = 0; x < NG; ++x) {
+    const int row = x * RPI + lane / PPR;
+    rowoff[x] = (uint32_t)(row * ROWB + (((lane % PPR) ^ swz(row)) << 4));
+  }
   auto issue = [&](unsigned char* tile, int step) {
     const int k0 = step * 32;
-    const int rr = lane / PPR;
-    const int slot = lane % PPR;
-#pragma unroll
-    for (int x = 0; x < NG; ++x) {
-      const int row = x * RPI + rr;
-      const uint16_t* src = row_of(k0 + row, kring, knew) + (slot ^ kswz(row)) * 8;
-      __builtin_amdgcn_global_load_lds((const void*)src,
-                                       (__attribute__((address_space(3))) void*)(tile + x * 1024),
-                                       16, 0, kPolicy);
-    }
-#pragma unroll
-    for (int x = 0; x < NG; ++x) {
-      const int row = x * RPI + rr;
-      const uint16_t* src = row_of(k0 + row, vring, vnew) + (slot ^ vswz(rr)) * 8;
+    auto dma = [&](const unsigned char* base, int x, uint32_t off, int vt) {
       __builtin_amdgcn_global_load_lds(
-          (const void*)src, (__attribute__((address_space(3))) void*)(tile + KTILE + x * VPITCH),
-          16, 0, kPolicy);
+          (const void*)(base + off),
+          (__attribute__((address_space(3))) void*)(tile + vt * TILE + x * 1024), 16, 0, kPolicy);
+    };
+    if (k0 + 31 < R.len0 || (k0 >= R.len0 && k0 + 31 < R.n_ring)) {
+      // The whole step lies in one slot range: rows are consecutive slots.
+      const int s0 = k0 < R.len0 ? R.base0 + k0 : k0 - R.len0;
+      const size_t sh = (size_t)s0 * ROWB;
+#pragma unroll
+      for (int x = 0; x < NG; ++x) dma(kring_b + sh, x, rowoff[x], 0);
+#pragma unroll
+      for (int x = 0; x < NG; ++x) dma(vring_b + sh, x, rowoff[x], 1);
+    } else {
+      // Per-lane slots: range boundary, current token (read from slot 0, replaced in LDS) or
+      // rows past the end (slot 0, masked).
+      uint32_t off[NG];
+#pragma unroll
+      for (int x = 0; x < NG; ++x) {
+        const int row = x * RPI + lane / PPR;
+        const int i = k0 + row;
+        const int slot = i < R.len0 ? R.base0 + i : (i < R.n_ring ? i - R.len0 : 0);
+        off[x] = (uint32_t)(slot * ROWB + (((lane % PPR) ^ swz(row)) << 4));
+      }
+#pragma unroll
+      for (int x = 0; x < NG; ++x) dma(kring_b, x, off[x], 0);
+#pragma unroll
+      for (int x = 0; x < NG; ++x) dma(vring_b, x, off[x], 1);
     }
   };
 
-  auto compute = [&](const unsigned char* tile, int step) {
+  // LDS read addresses (buffer 0 of this wave): K row operands (row c16, piece 4kk + j4; row
+  // 16 + c16 a fixed distance on) and transposed V reads of chunk nb (row 4j + c16/4, channels
+  // 16nb + 4(c16 mod 4) .. +3; rows 16.. a fixed distance on).
+  uint32_t kaddr[KK], vaddr[NB];
+  {
+    const uint32_t base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) unsigned char*)wbuf;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk)
+      kaddr[kk] = base + c16 * ROWB + (((4 * kk + j4) ^ swz(c16)) << 4);
+    const int r = 4 * j4 + (c16 >> 2);
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+      vaddr[nb] = base + TILE + r * ROWB + (((2 * nb + ((c16 & 3) >> 1)) ^ swz(r)) << 4) +
+                  ((c16 & 1) << 3);
+  }
+  const __attribute__((address_space(3))) unsigned char* lds0 = nullptr;
+  const float c = a.scale_log2;
+  const int cur_step = R.n_ring >> 5;   // the step that holds the current token
+
+  auto compute = [&](auto bi, int step) {
+    constexpr uint32_t BO = decltype(bi)::value * BUF;
     // This step's tiles have landed once at most the next step's OPS loads are outstanding.
     __builtin_amdgcn_s_waitcnt(0x0F70 | (OPS & 15) | ((OPS >> 4) << 14));
-    if constexpr (ROPE) {
-      // The current token's K row arrived unrotated from k_new: overwrite it with the turned
-      // key before the tile is read.
-      if (step == (R.n_ring >> 5)) {
-        const int rc = R.n_ring & 31;
+    if (step == cur_step) {
+      // The current token's row arrived from slot 0: overwrite it with k_new / v_new (the
+      // turned key in rotary mode).
+      const int rc = R.n_ring & 31;
+      unsigned char* tile = wbuf + BO;
+      if constexpr (ROPE) {
         if (lane < PPR / 2) {
-          unsigned char* row = (unsigned char*)tile + rc * ROWB;
-          *(u32x4*)(row + ((lane ^ kswz(rc)) << 4)) = krot_lo;
-          *(u32x4*)(row + (((lane + PPR / 2) ^ kswz(rc)) << 4)) = krot_hi;
+          unsigned char* row = tile + rc * ROWB;
+          *(u32x4*)(row + ((lane ^ swz(rc)) << 4)) = krot_lo;
+          *(u32x4*)(row + (((lane + PPR / 2) ^ swz(rc)) << 4)) = krot_hi;
         }
-        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        if (rowlane && lane >= PPR)
+          *(u32x4*)(tile + TILE + rc * ROWB + (((lane - PPR) ^ swz(rc)) << 4)) = cur_row;
+      } else if (rowlane) {
+        *(u32x4*)(tile + (lane >= PPR ? TILE : 0) + rc * ROWB + (((lane % PPR) ^ swz(rc)) << 4)) =
+            cur_row;
       }
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     }
     const int k0 = step * 32;
     f32x4 s0 = {0.0f, 0.0f, 0.0f, 0.0f};
     f32x4 s1 = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
-      const int p = 4 * kk + j4;
-      const bf16x8 ka = *(const bf16x8*)(tile + c16 * ROWB + ((p ^ kswz(c16)) << 4));
-      const bf16x8 kb = *(const bf16x8*)(tile + (16 + c16) * ROWB + ((p ^ kswz(16 + c16)) << 4));
+      const auto* p = lds0 + kaddr[kk] + BO;
+      const bf16x8 ka = *(const __attribute__((address_space(3))) bf16x8*)(p);
+      const bf16x8 kb = *(const __attribute__((address_space(3))) bf16x8*)(p + 16 * ROWB);
       s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qB[kk], s0, 0, 0, 0);
       s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb, qB[kk], s1, 0, 0, 0);
     }
-    float z[8];
+    // V^T reads go out now, under the softmax arithmetic.
+    u32x2 vr[2 * NB];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      z[e] = s0[e] * a.scale_log2;
-      z[4 + e] = s1[e] * a.scale_log2;
+    for (int nb = 0; nb < NB; ++nb) {
+      vr[2 * nb] = tr_read<BO>(vaddr[nb]);
+      vr[2 * nb + 1] = tr_read<BO + 16 * ROWB>(vaddr[nb]);
     }
-    float mx = kNegInf;
+    if (k0 + 32 > n_total) {
+      // Keys past the current token (the last step's padding) do not count.
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int key = k0 + (e < 4 ? 4 * j4 + e : 16 + 4 * j4 + (e - 4));
-      if (key >= n_total) z[e] = kNegInf;
-      mx = fmaxf(mx, z[e]);
+      for (int e = 0; e < 8; ++e) {
+        const int key = k0 + (e < 4 ? 4 * j4 + e : 16 + 4 * j4 + (e - 4));
+        if (key >= n_total) {
+          if (e < 4) s0[e] = kNegInf;
+          else s1[e - 4] = kNegInf;
+        }
+      }
     }
-    mx = fmaxf(mx, __shfl_xor(mx, 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float mn = fmaxf(m, mx);
-    const float alpha = fast_exp2(m - mn);  // 0 on the first step (m = -inf)
+    float mx = fmaxf(fmaxf(fmaxf(s0[0], s0[1]), fmaxf(s0[2], s0[3])),
+                     fmaxf(fmaxf(s1[0], s1[1]), fmaxf(s1[2], s1[3])));
+    mx = max_xor16_32(mx);
+    const float cand = mx * c;
+    const bool grow = cand > m + 8.0f;
+    if (__builtin_amdgcn_ballot_w64(grow) != 0) {
+      const float alpha = grow ? fast_exp2(m - cand) : 1.0f;   // 0 on the first step
+      m = grow ? cand : m;
+      lsum *= alpha;
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) acc[nb] *= alpha;
+    }
     float ps = 0.0f;
     bf16x8 pB;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      const float p = fast_exp2(z[e] - mn);
+      const float sc = e < 4 ? s0[e] : s1[e - 4];
+      const float p = fast_exp2(__builtin_fmaf(sc, c, -m));
       ps += p;
       pB[e] = (__bf16)p;
     }
-    lsum = lsum * alpha + ps;
-    m = mn;
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) acc[nb] *= alpha;
-    const unsigned char* vt = tile + KTILE;
+    lsum += ps;
+    if constexpr (NB == 8) {
+      asm volatile("s_waitcnt lgkmcnt(0)"
+                   : "+v"(vr[0]), "+v"(vr[1]), "+v"(vr[2]), "+v"(vr[3]), "+v"(vr[4]),
+                     "+v"(vr[5]), "+v"(vr[6]), "+v"(vr[7]), "+v"(vr[8]), "+v"(vr[9]),
+                     "+v"(vr[10]), "+v"(vr[11]), "+v"(vr[12]), "+v"(vr[13]), "+v"(vr[14]),
+                     "+v"(vr[15]));
+    } else {
+      asm volatile("s_waitcnt lgkmcnt(0)"
+                   : "+v"(vr[0]), "+v"(vr[1]), "+v"(vr[2]), "+v"(vr[3]), "+v"(vr[4]),
+                     "+v"(vr[5]), "+v"(vr[6]), "+v"(vr[7]));
+    }
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
-      const int col = 16 * nb + c16;
-      bf16x8 va;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int row = e < 4 ? 4 * j4 + e : 16 + 4 * j4 + (e - 4);
-        const int rr = row % RPI;
-        const int off = (row / RPI) * VPITCH + rr * ROWB + (((col >> 3) ^ vswz(rr)) << 4) +
-                        ((col & 7) << 1);
-        va[e] = *(const __bf16*)(vt + off);
-      }
-      acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pB, acc[nb], 0, 0, 0);
+      const u32x4 w = {vr[2 * nb][0], vr[2 * nb][1], vr[2 * nb + 1][0], vr[2 * nb + 1][1]};
+      acc[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, w), pB, acc[nb],
+                                                        0, 0, 0);
     }
   };
 
   // Two-deep software pipeline with a uniform trip count (pairs of steps), then the odd one.
   const int my_steps = wave < nsteps ? (nsteps - wave + NW - 1) / NW : 0;
   int step = wave;
-  issue(buf[0], step);
-  issue(buf[1], step + NW);
+  issue(wbuf, step);
+  issue(wbuf + BUF, step + NW);
   // Queries: wait until at most the two prefetched steps are outstanding, then read the
   // B operand (channels 32kk + 8j .. +7 of head c16; zero for padded heads).
   __builtin_amdgcn_s_waitcnt(0x0F70 | ((2 * OPS) & 15) | (((2 * OPS) >> 4) << 14));
@@ -532,25 +594,24 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
   }
   for (int pair = 0; pair < my_steps / 2; ++pair) {
     __builtin_amdgcn_sched_barrier(0);
-    compute(buf[0], step);
+    compute(std::integral_constant<int, 0>{}, step);
     __builtin_amdgcn_sched_barrier(0);
-    issue(buf[0], step + 2 * NW);
+    issue(wbuf, step + 2 * NW);
     step += NW;
     __builtin_amdgcn_sched_barrier(0);
-    compute(buf[1], step);
+    compute(std::integral_constant<int, 1>{}, step);
     __builtin_amdgcn_sched_barrier(0);
-    issue(buf[1], step + 2 * NW);
+    issue(wbuf + BUF, step + 2 * NW);
     step += NW;
   }
   if (my_steps & 1) {
     __builtin_amdgcn_sched_barrier(0);
-    compute(buf[0], step);
+    compute(std::integral_constant<int, 0>{}, step);
   }
   __builtin_amdgcn_s_waitcnt(0x0F70);  // drain the trailing prefetches before LDS is reused
 
   // l per head: sum the four quarters' partial sums.
-  lsum += __shfl_xor(lsum, 16);
-  lsum += __shfl_xor(lsum, 32);
+  lsum = sum_xor16_32(lsum);
 
   __syncthreads();  // every wave is done with its tiles: reuse LDS for the merge
   float* sm_acc = (float*)smem;              // [NW][16 heads][D]
@@ -569,7 +630,7 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
   __syncthreads();
   for (int idx = tid; idx < G * D; idx += NW * 64) {
     const int h = idx / D;
-    const int c = idx - h * D;
+    const int cc = idx - h * D;
     float M = kNegInf;
 #pragma unroll
     for (int w = 0; w < NW; ++w) M = fmaxf(M, sm_m[w * 16 + h]);
@@ -579,24 +640,26 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
       const float mw = sm_m[w * 16 + h];
       const float wt = (mw == kNegInf) ? 0.0f : fast_exp2(mw - M);
       L += wt * sm_l[w * 16 + h];
-      O += wt * sm_acc[(w * 16 + h) * D + c];
+      O += wt * sm_acc[(w * 16 + h) * D + cc];
     }
     out[idx] = float_to_bf16_rne(O / L);
   }
 
   // Fused append of the current token.  Slot t mod slots holds a position outside the support
   // of t (and of every later step), so no read of this launch can observe the write.
-  if constexpr (ROPE) {
-    if (wave == 0 && lane < PPR / 2) {
-      uint16_t* dst = kring + (size_t)R.append_slot * D;
-      *(u32x4*)(dst + lane * 8) = krot_lo;
-      *(u32x4*)(dst + D / 2 + lane * 8) = krot_hi;
+  if (wave == 0) {
+    if constexpr (ROPE) {
+      if (lane < PPR / 2) {
+        uint16_t* dst = kring + (size_t)R.append_slot * D;
+        *(u32x4*)(dst + lane * 8) = krot_lo;
+        *(u32x4*)(dst + D / 2 + lane * 8) = krot_hi;
+      }
+      if (rowlane && lane >= PPR)
+        *(u32x4*)(vring + (size_t)R.append_slot * D + (lane % PPR) * 8) = cur_row;
+    } else if (rowlane) {
+      *(u32x4*)((lane < PPR ? kring : vring) + (size_t)R.append_slot * D + (lane % PPR) * 8) =
+          cur_row;
     }
-    if (appender && lane >= PPR)
-      *(u32x4*)(vring + (size_t)R.append_slot * D + (lane % PPR) * 8) = append_row;
-  } else if (appender) {
-    *(u32x4*)((lane < PPR ? kring : vring) + (size_t)R.append_slot * D + (lane % PPR) * 8) =
-        append_row;
   }
 }
 
