@@ -7,12 +7,11 @@
 //   dv_s += p_s g_t
 //   ds_s  = p_s (g_t.v_s - delta_t),   delta_t = g_t.o_t
 //   dq_t  = scale sum_s ds_s k_s,      dk_s += scale ds_s q_t
-// summed over the query heads of each KV head for dk and dv.  Three launches:
-//   delta: lse * log2(e) and one fp32 dot product per (sequence, head, position) into the
-//          workspace;
+// summed over the query heads of each KV head for dk and dv.  Two launches:
 //   dq:    the prefill kernel's structure (128 query columns per workgroup, two 16-column
 //          groups per wave, walk their key interval in 32-key steps through LDS), no running
-//          maximum (lse is known);
+//          maximum (lse is known); each column also computes its delta and lse * log2(e) and
+//          writes them to the workspace for the second launch;
 //   dk/dv: transposed roles: each workgroup holds 64 keys of one KV head in registers and
 //          walks, for every query head of the group, the interval of targets whose supports
 //          contain those keys (PBB: up to h(floor(s/h) + 2) - 1; SWA: s + W - 1).
@@ -48,36 +47,6 @@ template <int D>
 __device__ __forceinline__ int dual_swz(int r) {
   if constexpr (D == 128) return 2 * (r & 7);
   return 2 * ((r >> 1) & 3);
-}
-
-// ------------------------------------------------------------------------------------------
-// Per (sequence, head, position): lse * log2(e) and delta = dout . out, into the workspace laid
-// out [batch][hq][2][n] (the two values of one (sequence, head) n floats apart).  One 16-lane
-// (d = 128) or 8-lane (d = 64) group per row.
-template <int D>
-__global__ __launch_bounds__(256) void bwd_delta_kernel(BackwardArgs a) {
-  constexpr int PPR = D / 8;
-  const size_t rows = (size_t)a.batch * a.n * a.hq;
-  const size_t row = (size_t)blockIdx.x * (256 / PPR) + threadIdx.x / PPR;
-  const int p = threadIdx.x % PPR;
-  float acc = 0.0f;
-  if (row < rows) {
-    const bf16x8 g = *(const bf16x8*)((const uint16_t*)a.dout + row * D + p * 8);
-    const bf16x8 o = *(const bf16x8*)((const uint16_t*)a.out + row * D + p * 8);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) acc = __builtin_fmaf((float)g[e], (float)o[e], acc);
-  }
-#pragma unroll
-  for (int m = PPR / 2; m >= 1; m >>= 1) acc += __shfl_xor(acc, m);
-  if (row < rows && p == 0) {
-    const size_t h = row % a.hq;
-    const size_t bt = row / a.hq;
-    const size_t t = bt % a.n;
-    const size_t b = bt / a.n;
-    float* w = a.ws + (b * a.hq + h) * 2 * (size_t)a.n;
-    w[t] = a.lse[(b * a.hq + h) * a.n + t] * 1.4426950408889634f;
-    w[a.n + t] = acc;
-  }
 }
 
 // Workgroup i runs on XCD i mod 8: give each XCD a contiguous run of tiles.
@@ -127,7 +96,7 @@ void bwd_dq_kernel(BackwardArgs a, int tq, int tiles) {
   int tc[QC], hc[QC], lo_c[QC], hi_c[QC];
   bool valid[QC];
   float lse2[QC], dlt[QC];
-  bf16x8 qB[QC][KK], gB[QC][KK];
+  bf16x8 qB[QC][KK], gB[QC][KK], oB[QC][KK];
 #pragma unroll
   for (int qc = 0; qc < QC; ++qc) {
     const int col = (wave * QC + qc) * 16 + c16;
@@ -140,17 +109,19 @@ void bwd_dq_kernel(BackwardArgs a, int tq, int tiles) {
     const size_t rowq = ((size_t)b * n + (valid[qc] ? tc[qc] : t0)) * a.hq + hc[qc];
     const uint16_t* qrow = (const uint16_t*)a.q + rowq * D;
     const uint16_t* grow = (const uint16_t*)a.dout + rowq * D;
+    const uint16_t* orow = (const uint16_t*)a.out + rowq * D;
     const u32x4 zero = {0u, 0u, 0u, 0u};
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
       const u32x4 wq = *(const u32x4*)(qrow + 32 * kk + 8 * j4);
       const u32x4 wg = *(const u32x4*)(grow + 32 * kk + 8 * j4);
+      const u32x4 wo = *(const u32x4*)(orow + 32 * kk + 8 * j4);
       qB[qc][kk] = __builtin_bit_cast(bf16x8, valid[qc] ? wq : zero);
       gB[qc][kk] = __builtin_bit_cast(bf16x8, valid[qc] ? wg : zero);
+      oB[qc][kk] = __builtin_bit_cast(bf16x8, valid[qc] ? wo : zero);
     }
-    const float* wrow = a.ws + ((size_t)b * a.hq + hc[qc]) * 2 * n + (valid[qc] ? tc[qc] : t0);
-    lse2[qc] = valid[qc] ? wrow[0] : 0.0f;
-    dlt[qc] = valid[qc] ? wrow[n] : 0.0f;
+    const float l = a.lse[((size_t)b * a.hq + hc[qc]) * n + (valid[qc] ? tc[qc] : t0)];
+    lse2[qc] = valid[qc] ? l * 1.4426950408889634f : 0.0f;
   }
 
   // DMA of key step st: rows k0 .. k0+31 of K then V (wave-uniform base at row k0, lane offset
@@ -206,6 +177,25 @@ void bwd_dq_kernel(BackwardArgs a, int tq, int tiles) {
   issue(0, 0);
   if (nsteps > 1) issue(1, 1);
   int rstage = 0;
+
+  // delta = dout . out of each column (the four quarters j hold channel slices 8j.. of every
+  // 32-channel block), and lse * log2(e): kept in registers for dq and written to the workspace
+  // for the dk/dv launch.
+#pragma unroll
+  for (int qc = 0; qc < QC; ++qc) {
+    float part = 0.0f;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk)
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        part = __builtin_fmaf((float)gB[qc][kk][e], (float)oB[qc][kk][e], part);
+    dlt[qc] = sum_xor16_32(part);
+    if (valid[qc] && j4 == 0) {
+      float* w = a.ws + ((size_t)b * a.hq + hc[qc]) * 2 * n + tc[qc];
+      w[0] = lse2[qc];
+      w[n] = dlt[qc];
+    }
+  }
 
   auto step = [&](int st, auto masked) {
     if (st + 1 < nsteps)
@@ -615,18 +605,12 @@ void bwd_dkdv_kernel(BackwardArgs a, int tiles) {
 
 template <int D>
 hipError_t launch_backward_d(const BackwardArgs& a, hipStream_t stream) {
-  constexpr int PPR = D / 8;
-  const size_t rows = (size_t)a.batch * a.n * a.hq;
-  const size_t dblocks = (rows + (256 / PPR) - 1) / (256 / PPR);
-  hipLaunchKernelGGL((bwd_delta_kernel<D>), dim3((unsigned)dblocks), dim3(256), 0, stream, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
   const int tq = (16 * kDqColGroups * kDqWaves) / a.group;
   const int qtiles = (a.n + tq - 1) / tq;
   hipLaunchKernelGGL((bwd_dq_kernel<D, kDqWaves, kDqColGroups>),
                      dim3((unsigned)((size_t)a.batch * a.hkv * qtiles)), dim3(kDqWaves * 64), 0,
                      stream, a, tq, qtiles);
-  e = hipGetLastError();
+  hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   constexpr int KT = 16 * kDkdvKeyGroups * kDkdvWaves;
   const int ktiles = (a.n + KT - 1) / KT;
