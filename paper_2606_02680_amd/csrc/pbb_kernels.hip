@@ -303,8 +303,7 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
   constexpr int TILE = 32 * ROWB;
   constexpr int BUF = 2 * TILE;         // one step: K tile then V tile
   constexpr int OPS = 2 * NG;           // DMA instructions per step
-  constexpr int QTILE = 16 * ROWB;      // the group's queries, 16 rows (heads >= G unused)
-  constexpr int STAGE_BYTES = NW * (2 * BUF + QTILE);
+  constexpr int STAGE_BYTES = NW * 2 * BUF;
   constexpr int MERGE_BYTES = NW * 16 * (D + 2) * 4;
   constexpr int SMEM = STAGE_BYTES > MERGE_BYTES ? STAGE_BYTES : MERGE_BYTES;
   __shared__ __align__(16) unsigned char smem[SMEM];
@@ -350,7 +349,6 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
   for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 
   unsigned char* const wbuf = smem + wave * 2 * BUF;   // this wave's two step buffers
-  unsigned char* qtile = smem + NW * 2 * BUF + wave * QTILE;
   const int nsteps = (n_total + 31) >> 5;
 
   // Rotary mode: queries and the new key are turned by position t inside this launch.  Their
@@ -376,19 +374,15 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
     for (int e = 0; e < 8; ++e) kturn[e] = a.rope_turns[8 * kl + e];
   }
 
-  // The group's query rows go to the wave's LDS query tile by the same DMA as K and V, ahead
-  // of the first K/V loads, so the first step's vmcnt wait covers them too (rows of heads
-  // >= G repeat head G-1 and are zeroed when read).
+  // The group's queries as the B operand (channels 32kk + 8j .. +7 of head c16), loaded into
+  // registers ahead of the first K/V loads so that the first step's vmcnt wait covers them
+  // (lanes of heads >= G load head G-1 and are zeroed when used).
+  u32x4 qload[ROPE ? 1 : KK];
   if constexpr (!ROPE) {
-    const uint16_t* qbase = (const uint16_t*)a.q + ((size_t)b * a.hq + (size_t)g * G) * D;
+    const uint16_t* qrow = (const uint16_t*)a.q + ((size_t)b * a.hq + (size_t)g * G +
+                                                   (size_t)(c16 < G ? c16 : G - 1)) * D;
 #pragma unroll
-    for (int x = 0; x < 16 / RPI; ++x) {
-      const int h = x * RPI + lane / PPR;
-      const uint16_t* src = qbase + (size_t)(h < G ? h : G - 1) * D + (lane % PPR) * 8;
-      __builtin_amdgcn_global_load_lds((const void*)src,
-                                       (__attribute__((address_space(3))) void*)(qtile + x * 1024),
-                                       16, 0, 0);
-    }
+    for (int kk = 0; kk < KK; ++kk) qload[kk] = *(const u32x4*)(qrow + 32 * kk + 8 * j4);
   }
 
   // DMA of one step.  Lane l loads 16-byte piece (l mod PPR) ^ swz(row) of rows
@@ -551,8 +545,8 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
   int step = wave;
   issue(wbuf, step);
   issue(wbuf + BUF, step + NW);
-  // Queries: wait until at most the two prefetched steps are outstanding, then read the
-  // B operand (channels 32kk + 8j .. +7 of head c16; zero for padded heads).
+  // Queries: wait until at most the two prefetched steps are outstanding (zero for padded
+  // heads).
   __builtin_amdgcn_s_waitcnt(0x0F70 | ((2 * OPS) & 15) | (((2 * OPS) >> 4) << 14));
   if constexpr (ROPE) {
     // Turn the queries (channel 32kk + 8j + e pairs with the same channel of slice kk + KK/2)
@@ -589,8 +583,7 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
 #pragma unroll
   for (int kk = 0; kk < (ROPE ? 0 : KK); ++kk) {
     const u32x4 zero = {0u, 0u, 0u, 0u};
-    const u32x4 w = *(const u32x4*)(qtile + c16 * ROWB + (4 * kk + j4) * 16);
-    qB[kk] = __builtin_bit_cast(bf16x8, c16 < G ? w : zero);
+    qB[kk] = __builtin_bit_cast(bf16x8, c16 < G ? qload[kk] : zero);
   }
   for (int pair = 0; pair < my_steps / 2; ++pair) {
     __builtin_amdgcn_sched_barrier(0);
