@@ -119,7 +119,16 @@ pbb_status_t pbb_ring_fill(const pbb_desc_t *desc, const int32_t *pos, const voi
                            const void *v_src, int32_t src_len, void *k_ring, void *v_ring,
                            void *stream);
 
-/* Workspace bytes pbb_decode_step needs (0 when the selected kernel needs none). */
+/*
+ * Workspace bytes pbb_decode_step needs.  0 unless the launch is split: bf16 launches with at
+ * most 32 (sequence, KV head) units and supports of at least 32 32-key steps spread each unit's
+ * support over several workgroups,
+ * which leave partial softmax states (Eq.(lse), Appendix A.4) in the workspace for the last of
+ * them to merge.  Its first 256-byte-aligned part holds one counter per unit: it must be
+ * zero-filled before the first call, and every call leaves it zero again, so one allocation
+ * serves every later call on one stream; calls that may run concurrently need separate
+ * workspaces.  The size depends only on the descriptor.
+ */
 pbb_status_t pbb_workspace_bytes(const pbb_desc_t *desc, size_t *bytes);
 
 /*
@@ -131,13 +140,14 @@ pbb_status_t pbb_workspace_bytes(const pbb_desc_t *desc, size_t *bytes);
  *      (Eq.(pbb) with h = B/2, Eq.(attention)).
  * Requires slots == block and window ignored.  pos is read, never written: the caller
  * advances it (for example pos += 1 on the same stream) before the next step.
- * workspace may be NULL when pbb_workspace_bytes reports 0.
+ * workspace: pbb_workspace_bytes bytes, 16-byte aligned, zero-filled before first use; may be
+ * NULL when that is 0 (PBB_ERR_WORKSPACE if NULL or smaller otherwise).
  */
 pbb_status_t pbb_decode_step(const pbb_desc_t *desc, const int32_t *pos, const void *q,
                              const void *k_new, const void *v_new, void *k_ring, void *v_ring,
                              void *out, void *workspace, size_t workspace_bytes, void *stream);
 
-/* Workspace bytes swa_decode_step needs (0 when the selected kernel needs none). */
+/* Workspace bytes swa_decode_step needs (the rules of pbb_workspace_bytes). */
 pbb_status_t swa_workspace_bytes(const pbb_desc_t *desc, size_t *bytes);
 
 /*

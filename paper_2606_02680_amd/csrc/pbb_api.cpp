@@ -6,6 +6,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 
@@ -16,6 +17,8 @@ namespace {
 constexpr int32_t kMaxGroup = 16;     // query heads per KV head held by one MFMA tile
 constexpr int32_t kMaxSlots = 65536;  // ring slots per (sequence, KV head)
 constexpr int32_t kMaxPrefill = 1 << 30;  // prompt positions per call
+constexpr int64_t kSplitUnits = 256;      // workgroups a split decode launch aims for (CUs)
+constexpr int64_t kSplitMaxUnits = 32;    // bf16 decode launches with at most this many units split
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
@@ -49,12 +52,36 @@ size_t ring_tensor_bytes(const pbb_desc_t* d) {
          elem_bytes(d->dtype);
 }
 
+// Workgroups per (sequence, KV head) unit of a bf16 decode launch: launches with few units
+// spread each unit's key steps over several workgroups (at least 16 32-key steps, four per wave
+// of a 4-wave workgroup), so that more of the chip streams the rings.  The merge through the
+// workspace costs three serial device-coherent round trips (~5 us), which only pays off for
+// small batches with long supports.
+int32_t decode_splits(const pbb_desc_t* d, bool swa) {
+  if (d->dtype != PBB_DTYPE_BF16) return 1;
+  const int64_t units = (int64_t)d->batch * d->n_kv_heads;
+  if (units > kSplitMaxUnits) return 1;
+  const int64_t max_steps = ((int64_t)(swa ? d->window : d->block) + 31) / 32;
+  const int64_t s = std::min((kSplitUnits + units - 1) / units, (max_steps + 15) / 16);
+  return (int32_t)std::max<int64_t>(1, s);
+}
+
+size_t counters_bytes(const pbb_desc_t* d) {
+  return ((size_t)d->batch * (size_t)d->n_kv_heads * 4 + 255) / 256 * 256;
+}
+
+size_t decode_workspace(const pbb_desc_t* d, bool swa) {
+  const int32_t s = decode_splits(d, swa);
+  if (s <= 1) return 0;
+  const size_t part = (size_t)d->batch * (size_t)d->n_kv_heads * (size_t)s *
+                      (size_t)(d->n_q_heads / d->n_kv_heads) * (size_t)(d->head_dim + 2) * 4;
+  return counters_bytes(d) + (part + 255) / 256 * 256;
+}
+
 pbb_status_t decode_common(const pbb_desc_t* desc, bool swa, const int32_t* pos, int32_t* pos_next,
                            bool want_next, const void* q, const void* k_new, const void* v_new,
                            void* k_ring, void* v_ring, void* out, void* workspace,
                            size_t workspace_bytes, void* stream) {
-  (void)workspace;
-  (void)workspace_bytes;  // the selected kernels need no workspace
   const pbb_status_t st = check_desc(desc, swa);
   if (st != PBB_OK) return st;
   if (!pos || !q || !k_new || !v_new || !k_ring || !v_ring || !out) return PBB_ERR_NULL;
@@ -67,8 +94,16 @@ pbb_status_t decode_common(const pbb_desc_t* desc, bool swa, const int32_t* pos,
   if (!aligned(pos, 4) || !aligned(q, 16) || !aligned(k_new, 16) || !aligned(v_new, 16) ||
       !aligned(k_ring, 16) || !aligned(v_ring, 16) || !aligned(out, 16))
     return PBB_ERR_ALIGN;
+  const size_t need = decode_workspace(desc, swa);
+  if (need > 0 && (workspace == nullptr || workspace_bytes < need)) return PBB_ERR_WORKSPACE;
+  if (need > 0 && !aligned(workspace, 16)) return PBB_ERR_ALIGN;
 
   pbb::DecodeArgs a;
+  a.splits = need > 0 ? decode_splits(desc, swa) : 1;
+  a.counters = need > 0 ? static_cast<uint32_t*>(workspace) : nullptr;
+  a.ws_part = need > 0 ? reinterpret_cast<float*>(static_cast<unsigned char*>(workspace) +
+                                                  counters_bytes(desc))
+                       : nullptr;
   a.pos = pos;
   a.pos_next = want_next ? pos_next : nullptr;
   a.q = q;
@@ -266,7 +301,7 @@ pbb_status_t pbb_workspace_bytes(const pbb_desc_t* desc, size_t* bytes) {
   if (desc == nullptr || bytes == nullptr) return PBB_ERR_NULL;
   const pbb_status_t st = check_desc(desc, false);
   if (st != PBB_OK) return st;
-  *bytes = 0;
+  *bytes = decode_workspace(desc, false);
   return PBB_OK;
 }
 
@@ -274,7 +309,7 @@ pbb_status_t swa_workspace_bytes(const pbb_desc_t* desc, size_t* bytes) {
   if (desc == nullptr || bytes == nullptr) return PBB_ERR_NULL;
   const pbb_status_t st = check_desc(desc, true);
   if (st != PBB_OK) return st;
-  *bytes = 0;
+  *bytes = decode_workspace(desc, true);
   return PBB_OK;
 }
 

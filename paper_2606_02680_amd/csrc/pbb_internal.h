@@ -30,6 +30,13 @@ struct DecodeArgs {
   int32_t mode;        // SupportMode
   float scale_log2;    // softmax scale times log2(e)
   int32_t rope;        // 1: rotate q and the new key by their position (rotary embedding)
+  // Split of each unit's key steps over `splits` workgroups (1: none).  With splits > 1 the
+  // workgroups of a unit leave partial states (unnormalised output, maximum and sum per head)
+  // in ws_part and count in counters[unit]; the last to arrive merges them (Eq.(lse)) and
+  // resets the counter to 0.
+  int32_t splits;
+  uint32_t* counters;  // [batch * hkv], zero between launches
+  float* ws_part;      // [batch * hkv][splits][group][head_dim + 2]
   // Turns per position of rotary channel pair c (angle / 2 pi), c < head_dim / 2.
   double rope_turns[64];
 };

@@ -291,7 +291,16 @@ __global__ __launch_bounds__(256) void decode_f32_kernel(DecodeArgs a) {
 // 256-byte rows and 2 ((r >> 1) mod 4) for 128-byte rows: both the 16-byte row reads of the
 // scores and the transposed reads of the values hit distinct banks within every group of lanes
 // that gfx950 serves per cycle.
-template <int D, int NW, bool NT, bool ROPE>
+// Device-coherent float store and load (agent scope): they bypass the caches that are not
+// coherent across the chip's compute dies, without writing back or invalidating those caches.
+__device__ __forceinline__ void coherent_store(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float coherent_load(const float* p) {
+  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+template <int D, int NW, bool NT, bool ROPE, bool SPLIT>
 __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
   constexpr int kPolicy = NT ? kCachePolicyNT : 0;
   constexpr int KK = D / 32;            // 32-channel slices of the score contraction
@@ -305,10 +314,12 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
   constexpr int OPS = 2 * NG;           // DMA instructions per step
   constexpr int STAGE_BYTES = NW * 2 * BUF;
   constexpr int MERGE_BYTES = NW * 16 * (D + 2) * 4;
-  constexpr int SMEM = STAGE_BYTES > MERGE_BYTES ? STAGE_BYTES : MERGE_BYTES;
+  constexpr int SMEM = STAGE_BYTES > MERGE_BYTES + 16 ? STAGE_BYTES : MERGE_BYTES + 16;
   __shared__ __align__(16) unsigned char smem[SMEM];
 
-  const int bg = blockIdx.x;
+  const int S = SPLIT ? a.splits : 1;
+  const int bg = blockIdx.x / S;        // unit: (sequence, KV head)
+  const int sp = blockIdx.x - bg * S;   // this workgroup's share of the unit's steps
   const int b = bg / a.hkv;
   const int g = bg - b * a.hkv;
   const int tid = threadIdx.x;
@@ -320,8 +331,9 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
   uint16_t* out = (uint16_t*)a.out + ((size_t)b * a.hq + (size_t)g * G) * D;
   const int t = a.pos[b];
   if (t < 0) {
-    for (int e = tid; e < G * D; e += NW * 64) out[e] = 0;
-    if (a.pos_next != nullptr && g == 0 && tid == 0) a.pos_next[b] = t;
+    if (sp == 0)
+      for (int e = tid; e < G * D; e += NW * 64) out[e] = 0;
+    if (a.pos_next != nullptr && g == 0 && sp == 0 && tid == 0) a.pos_next[b] = t;
     return;
   }
   const Ranges R = ranges_for(a, t);
@@ -330,7 +342,7 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
   uint16_t* vring = (uint16_t*)a.v_ring + (size_t)bg * a.slots * D;
   const uint16_t* knew = (const uint16_t*)a.k_new + (size_t)bg * D;
   const uint16_t* vnew = (const uint16_t*)a.v_new + (size_t)bg * D;
-  if (a.pos_next != nullptr && g == 0 && tid == 0) a.pos_next[b] = t + 1;
+  if (a.pos_next != nullptr && g == 0 && sp == 0 && tid == 0) a.pos_next[b] = t + 1;
 
   auto swz = [](int r) -> int { return D == 128 ? 2 * (r & 7) : 2 * ((r >> 1) & 3); };
 
@@ -350,6 +362,11 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
 
   unsigned char* const wbuf = smem + wave * 2 * BUF;   // this wave's two step buffers
   const int nsteps = (n_total + 31) >> 5;
+  // Steps [st_lo, st_hi) of the unit belong to this workgroup.
+  const int st_lo = SPLIT ? (int)(((long long)sp * nsteps) / S) : 0;
+  const int st_hi = SPLIT ? (int)(((long long)(sp + 1) * nsteps) / S) : nsteps;
+  // later rows are only read to keep the wait counts fixed
+  const int k_lim = SPLIT ? st_hi * 32 : 0x7fffffff;
 
   // Rotary mode: queries and the new key are turned by position t inside this launch.  Their
   // raw values and the per-channel turn rates are loaded into registers here, before any K/V
@@ -402,7 +419,7 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
           (const void*)(base + off),
           (__attribute__((address_space(3))) void*)(tile + vt * TILE + x * 1024), 16, 0, kPolicy);
     };
-    if (k0 + 31 < R.len0 || (k0 >= R.len0 && k0 + 31 < R.n_ring)) {
+    if (k0 < k_lim && (k0 + 31 < R.len0 || (k0 >= R.len0 && k0 + 31 < R.n_ring))) {
       // The whole step lies in one slot range: rows are consecutive slots.
       const int s0 = k0 < R.len0 ? R.base0 + k0 : k0 - R.len0;
       const size_t sh = (size_t)s0 * ROWB;
@@ -412,13 +429,13 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
       for (int x = 0; x < NG; ++x) dma(vring_b + sh, x, rowoff[x], 1);
     } else {
       // Per-lane slots: range boundary, current token (read from slot 0, replaced in LDS) or
-      // rows past the end (slot 0, masked).
+      // rows past this workgroup's steps (slot 0, never used).
       uint32_t off[NG];
 #pragma unroll
       for (int x = 0; x < NG; ++x) {
         const int row = x * RPI + lane / PPR;
         const int i = k0 + row;
-        const int slot = i < R.len0 ? R.base0 + i : (i < R.n_ring ? i - R.len0 : 0);
+        const int slot = (k0 >= k_lim || i >= R.n_ring) ? 0 : (i < R.len0 ? R.base0 + i : i - R.len0);
         off[x] = (uint32_t)(slot * ROWB + (((lane % PPR) ^ swz(row)) << 4));
       }
 #pragma unroll
@@ -541,8 +558,8 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
   };
 
   // Two-deep software pipeline with a uniform trip count (pairs of steps), then the odd one.
-  const int my_steps = wave < nsteps ? (nsteps - wave + NW - 1) / NW : 0;
-  int step = wave;
+  const int my_steps = wave < st_hi - st_lo ? (st_hi - st_lo - wave + NW - 1) / NW : 0;
+  int step = st_lo + wave;
   issue(wbuf, step);
   issue(wbuf + BUF, step + NW);
   // Queries: wait until at most the two prefetched steps are outstanding (zero for padded
@@ -621,6 +638,8 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
     }
   }
   __syncthreads();
+  // This workgroup's state per head: reference M (log2 units), sum L, unnormalised output O.
+  float* part = SPLIT ? a.ws_part + ((size_t)bg * S + sp) * G * (D + 2) : nullptr;
   for (int idx = tid; idx < G * D; idx += NW * 64) {
     const int h = idx / D;
     const int cc = idx - h * D;
@@ -635,12 +654,54 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
       L += wt * sm_l[w * 16 + h];
       O += wt * sm_acc[(w * 16 + h) * D + cc];
     }
-    out[idx] = float_to_bf16_rne(O / L);
+    if constexpr (!SPLIT) {
+      out[idx] = float_to_bf16_rne(O / L);
+    } else {
+      coherent_store(part + idx, O);
+      if (cc == 0) {
+        coherent_store(part + G * D + h, M);
+        coherent_store(part + G * D + G + h, L);
+      }
+    }
+  }
+  if constexpr (SPLIT) {
+    // The last of the unit's workgroups to finish merges all S states (Eq.(lse)) and resets
+    // the unit's counter for the next launch.  The states travel through device-coherent
+    // stores and loads; every store of this workgroup has completed (the wait below, then the
+    // barrier) before its count is added, so the workgroup that observes the final count
+    // reads complete states.  No cache-wide write-back or invalidation is involved.
+    int* last = (int*)(smem + MERGE_BYTES);
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this thread's stores have completed
+    __syncthreads();
+    if (tid == 0)
+      *last = __hip_atomic_fetch_add(&a.counters[bg], 1u, __ATOMIC_RELAXED,
+                                     __HIP_MEMORY_SCOPE_AGENT) == (unsigned)(S - 1) ? 1 : 0;
+    __syncthreads();
+    if (*last) {
+      const float* p0 = a.ws_part + (size_t)bg * S * G * (D + 2);
+      for (int idx = tid; idx < G * D; idx += NW * 64) {
+        const int h = idx / D;
+        float M = kNegInf;
+        for (int s = 0; s < S; ++s) M = fmaxf(M, coherent_load(p0 + (size_t)s * G * (D + 2) + G * D + h));
+        float L = 0.0f, O = 0.0f;
+        for (int s = 0; s < S; ++s) {
+          const float* ps = p0 + (size_t)s * G * (D + 2);
+          const float ms = coherent_load(ps + G * D + h);
+          const float wt = (ms == kNegInf) ? 0.0f : fast_exp2(ms - M);
+          L += wt * coherent_load(ps + G * D + G + h);
+          O += wt * coherent_load(ps + idx);
+        }
+        out[idx] = float_to_bf16_rne(O / L);
+      }
+      if (tid == 0)
+        __hip_atomic_store(&a.counters[bg], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
   }
 
-  // Fused append of the current token.  Slot t mod slots holds a position outside the support
-  // of t (and of every later step), so no read of this launch can observe the write.
-  if (wave == 0) {
+  // Fused append of the current token (by the unit's first workgroup).  Slot t mod slots holds
+  // a position outside the support of t (and of every later step), so no read of this launch
+  // can observe the write.
+  if (wave == 0 && sp == 0) {
     if constexpr (ROPE) {
       if (lane < PPR / 2) {
         uint16_t* dst = kring + (size_t)R.append_slot * D;
@@ -688,14 +749,24 @@ hipError_t launch_ring_fill(const int32_t* pos, const void* k_src, const void* v
 
 template <int D, int NW>
 void launch_bf16_policy(const DecodeArgs& a, bool nt, hipStream_t stream) {
-  const dim3 grid((unsigned)(a.batch * a.hkv));
+  const dim3 grid((unsigned)(a.batch * a.hkv * a.splits));
   const dim3 block(NW * 64);
+  if (a.splits > 1) {
+    if (a.rope) {
+      if (nt) hipLaunchKernelGGL((decode_bf16_kernel<D, NW, true, true, true>), grid, block, 0, stream, a);
+      else hipLaunchKernelGGL((decode_bf16_kernel<D, NW, false, true, true>), grid, block, 0, stream, a);
+    } else {
+      if (nt) hipLaunchKernelGGL((decode_bf16_kernel<D, NW, true, false, true>), grid, block, 0, stream, a);
+      else hipLaunchKernelGGL((decode_bf16_kernel<D, NW, false, false, true>), grid, block, 0, stream, a);
+    }
+    return;
+  }
   if (a.rope) {
-    if (nt) hipLaunchKernelGGL((decode_bf16_kernel<D, NW, true, true>), grid, block, 0, stream, a);
-    else hipLaunchKernelGGL((decode_bf16_kernel<D, NW, false, true>), grid, block, 0, stream, a);
+    if (nt) hipLaunchKernelGGL((decode_bf16_kernel<D, NW, true, true, false>), grid, block, 0, stream, a);
+    else hipLaunchKernelGGL((decode_bf16_kernel<D, NW, false, true, false>), grid, block, 0, stream, a);
   } else {
-    if (nt) hipLaunchKernelGGL((decode_bf16_kernel<D, NW, true, false>), grid, block, 0, stream, a);
-    else hipLaunchKernelGGL((decode_bf16_kernel<D, NW, false, false>), grid, block, 0, stream, a);
+    if (nt) hipLaunchKernelGGL((decode_bf16_kernel<D, NW, true, false, false>), grid, block, 0, stream, a);
+    else hipLaunchKernelGGL((decode_bf16_kernel<D, NW, false, false, false>), grid, block, 0, stream, a);
   }
 }
 

@@ -154,8 +154,8 @@ def swa_workspace_bytes(desc: PbbDesc) -> int:
 
 def alloc_workspace(desc: PbbDesc, device="cuda"):
     """Zero-filled workspace for the decode calls of ``desc`` (PBB or SWA rules by
-    ``desc.window``), or None when they need none.  Launches leave it zeroed, so one allocation
-    serves every later call on one stream."""
+    ``desc.window``), or None when they need none.  Launches leave its counters zeroed, so one
+    allocation serves every later call on one stream (calls that may overlap need their own)."""
     n = swa_workspace_bytes(desc) if desc.window > 0 else workspace_bytes(desc)
     return torch.zeros(n, dtype=torch.uint8, device=device) if n > 0 else None
 
@@ -203,6 +203,10 @@ def _decode(fn: str, desc: PbbDesc, pos, q, k_new, v_new, k_ring, v_ring, out, w
         _expect(n, t, (desc.batch, desc.n_kv_heads, desc.head_dim), desc.torch_dtype)
     for n, t in (("k_ring", k_ring), ("v_ring", v_ring)):
         _expect(n, t, ring_shape(desc), desc.torch_dtype)
+    if workspace is None:
+        # a fresh zero-filled workspace when the launch needs one (split workgroups); callers
+        # that capture graphs or step in a loop pass their own from alloc_workspace
+        workspace = alloc_workspace(desc, q.device)
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     extra = () if pos_next is None else (_ptr(pos_next),)
     _check(fn, getattr(load_library(), fn)(

@@ -247,3 +247,26 @@ def test_backward_argument_errors(fn):
     assert _backward(f32, fn) == 3
     assert _backward(_desc(rope_base=1e6), "pbb_backward") == 2
     assert _backward(desc, fn, n=0, ws=0) == 0
+
+
+def test_split_decode_workspace():
+    """bf16 launches with at most 32 (sequence, KV head) units split each unit over several
+    workgroups and need a workspace: counters (256-byte aligned) plus partial states."""
+    one = B.make_desc(1, 32, 8, 128, block=2048, dtype=torch.bfloat16)
+    # 8 units -> min(ceil(256 / 8), ceil(64 / 16)) = 4 workgroups per unit
+    assert P.workspace_bytes(one) == 256 + 8 * 4 * 4 * (128 + 2) * 4
+    swa = B.make_desc(2, 8, 2, 128, window=4096, slots=4096, dtype=torch.bfloat16)
+    assert P.swa_workspace_bytes(swa) == 256 + 4 * min(64, 8) * 4 * 130 * 4
+    many = B.make_desc(5, 32, 8, 128, block=2048, dtype=torch.bfloat16)   # 40 units
+    assert P.workspace_bytes(many) == 0
+    short = B.make_desc(1, 32, 8, 128, block=256, dtype=torch.bfloat16)   # 8 steps at most
+    assert P.workspace_bytes(short) == 0
+    f32 = B.make_desc(1, 32, 8, 128, block=2048, dtype=torch.float32)
+    assert P.workspace_bytes(f32) == 0
+    # a split launch without (or with too small) a workspace is refused before launching
+    vp = ctypes.c_void_p
+    lib = B.load_library()
+    args = [ctypes.byref(one), vp(A), vp(A), vp(A), vp(A), vp(A), vp(A), vp(A)]
+    assert lib.pbb_decode_step(*args, vp(0), ctypes.c_size_t(0), vp(0)) == 5
+    assert lib.pbb_decode_step(*args, vp(A), ctypes.c_size_t(P.workspace_bytes(one) - 1), vp(0)) == 5
+    assert lib.pbb_decode_step(*args, vp(A + 8), ctypes.c_size_t(1 << 24), vp(0)) == 4

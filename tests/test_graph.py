@@ -160,3 +160,54 @@ def test_advance_variant_matches_plain_steps(cuda, mode):
         g.replay()
         torch.cuda.synchronize()
         check(f"replay {rep}")
+
+
+def test_graph_replay_with_split_workgroups(cuda):
+    """A split launch (one sequence at c3's head shapes: each unit over 4 workgroups that merge
+    through the workspace, whose counters every launch leaves at zero) captured as a 48-step
+    graph with on-device position advance: every replay reproduces eager execution bit for
+    bit."""
+    steps = 48
+    cfg = W.Config("split-graph", "pbb", batch=1, hq=32, hkv=8, d=128, block=2048, slots=2048,
+                   window=0, dtype="bf16", seed=17, value_scale=1.0, pos_hi=200000, steps=steps,
+                   prefill=True)
+    t0 = W.initial_positions(cfg)
+    run = Run(cfg, t0, steps, cuda)
+    ws = run.ws
+    assert ws is not None and ws.numel() > 0
+    qs = W.q_steps(cfg, t0, 0, steps, device=cuda)
+    ks = W.kv_steps(cfg, "k", t0, 0, steps, device=cuda)
+    vs = W.kv_steps(cfg, "v", t0, 0, steps, device=cuda)
+    snap = (run.k_ring.clone(), run.v_ring.clone())
+    pos = [run.pos.clone(), torch.zeros_like(run.pos)]
+    eager = torch.empty_like(qs)
+    for i in range(steps):
+        P.pbb_decode_step_advance(run.desc, pos[i % 2], pos[(i + 1) % 2], qs[i], ks[i], vs[i],
+                                  run.k_ring, run.v_ring, eager[i], workspace=ws)
+    torch.cuda.synchronize()
+    ref_k, ref_v = run.k_ring.clone(), run.v_ring.clone()
+    outs = torch.zeros_like(qs)
+
+    def restore():
+        run.k_ring.copy_(snap[0])
+        run.v_ring.copy_(snap[1])
+        pos[0].copy_(run.t0.to(torch.int32).to(cuda))
+
+    restore()
+    g = torch.cuda.CUDAGraph()
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        for i in range(steps):
+            P.pbb_decode_step_advance(run.desc, pos[i % 2], pos[(i + 1) % 2], qs[i], ks[i], vs[i],
+                                      run.k_ring, run.v_ring, outs[i], workspace=ws)
+    for rep in range(3):
+        restore()
+        outs.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(outs.view(torch.int16), eager.view(torch.int16)), rep
+        assert torch.equal(run.k_ring.view(torch.int16), ref_k.view(torch.int16)), rep
+        assert torch.equal(run.v_ring.view(torch.int16), ref_v.view(torch.int16)), rep
+        assert not ws[: 4 * cfg.batch * cfg.hkv].any().item()
+        _ = (qs[0].float() * 2).sum().item()

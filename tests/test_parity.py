@@ -233,3 +233,35 @@ def test_snapshot_restore_continues_bitwise(cuda):
     outs_b = [run.step()[1].clone() for _ in range(300)]
     for x, y in zip(outs_a, outs_b):
         assert torch.equal(x.view(torch.int16), y.view(torch.int16))
+
+
+@pytest.mark.parametrize("mode,batch,d,hq,hkv,block,window,slots,pos_hi,steps", [
+    ("pbb", 1, 128, 32, 8, 2048, 0, 2048, 300000, 6),   # c3's heads, one sequence: 4 splits
+    ("pbb", 1, 128, 32, 8, 2048, 0, 2048, 0, 40),       # from position 0: mostly empty splits
+    ("pbb", 3, 64, 12, 2, 1024, 0, 1024, 5000, 8),      # 2 splits
+    ("swa", 2, 128, 8, 2, 0, 4096, 4096, 300000, 4),    # 8 splits
+])
+def test_split_workgroups_small_batch(cuda, mode, batch, d, hq, hkv, block, window, slots,
+                                      pos_hi, steps):
+    """Launches with fewer (sequence, KV head) units than CUs spread each unit's steps over
+    several workgroups, which merge their softmax states (Eq.(lse)) in the last to finish:
+    every sequence at every step against the oracle, rings bit for bit."""
+    cfg = W.Config(f"split-{mode}-{batch}-{d}-{hq}-{hkv}-{block}-{window}-{pos_hi}", mode,
+                   batch=batch, hq=hq, hkv=hkv, d=d, block=block, slots=slots, window=window,
+                   dtype="bf16", seed=13, value_scale=1.0, pos_hi=pos_hi, steps=steps,
+                   prefill=pos_hi > 0)
+    t0 = W.initial_positions(cfg)
+    run = Run(cfg, t0, steps, cuda)
+    assert run.ws is not None and run.ws.numel() > 0, "expected a split launch"
+    rows = np.arange(batch)
+    hist = run.history(rows, steps - 1)
+    print(f"[split] {cfg.name} t0={t0.tolist()}", flush=True)
+    for i in range(steps):
+        q, out = run.step()
+        compare(cfg, to_np(out), run.oracle_out(rows, i, q, hist=hist), what=f"{cfg.name} step {i}")
+    for which in ("k", "v"):
+        exp = run.expected_ring(rows, steps - 1, which, hist=hist)
+        assert np.array_equal(run.ring_rows(rows, which), exp), f"{cfg.name} ring {which}"
+    # the launches left every unit counter at zero
+    units = batch * hkv
+    assert not run.ws[: 4 * units].any().item()
