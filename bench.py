@@ -8,7 +8,8 @@ Inputs are seeded synthetic tensors already resident in HBM; rings are pre-fille
 Default workload (c3): batch 256, Hq 32, Hkv 8, head_dim 128, B 2048, bf16, positions
 uniform in [0, 512K).  Also reported: the same-library sliding-window ring on the same
 tensors (W = 2B = 4096 in 4096 slots, plus the paper-matched W = B), the ragged GQA-8
-workload (c4), the paper-shape latency sweep, and prefill (PBB and SWA) in TFLOP/s against
+workload (c4), the paper-shape latency sweep, small-batch latency at c3's head shapes, and
+prefill (PBB and SWA) in TFLOP/s against
 the bf16 matrix-core peak, and the training backward of the same shapes.
 
 Prints ONE JSON line.  Roofline: algorithmic bytes of the support actually read (ring K and
@@ -277,6 +278,51 @@ BACKWARD_SHAPES = tuple((name.replace("prefill", "backward"), shape)
 
 def backward_extras(device):
     return {name: backward_measure(device, **shape) for name, shape in BACKWARD_SHAPES}
+
+
+def small_batch_latency(device, batches=(1, 4), steps=64, reps=7):
+    """Decode latency at c3's head shapes (B 2048; SWA W 4096 in 4096 slots) for small batches,
+    where a launch has few (sequence, KV head) units and is split over workgroups: 64 steps of
+    ``*_decode_step_advance`` captured as one HIP graph, median replay time / 64."""
+    import statistics
+    import torch
+    import paper_2606_02680_amd as P
+    import workloads as W
+    res = {}
+    for batch in batches:
+        for name in ("c3", "c5"):
+            cfg = W.get_config(name).with_(batch=batch)
+            t0 = W.initial_positions(cfg)
+            wl = Workload(cfg, t0, steps, device)
+            qs, ks, vs = wl.inputs
+            adv = P.swa_decode_step_advance if cfg.mode == "swa" else P.pbb_decode_step_advance
+            pos = [wl.pos.clone(), torch.zeros_like(wl.pos)]
+            out = torch.empty_like(qs[0])
+            snap = (wl.k_ring.clone(), wl.v_ring.clone())
+            g = torch.cuda.CUDAGraph()
+            torch.cuda.synchronize()
+            with torch.cuda.graph(g):
+                for i in range(steps):
+                    adv(wl.desc, pos[i % 2], pos[(i + 1) % 2], qs[i], ks[i], vs[i], wl.k_ring,
+                        wl.v_ring, out, wl.ws)
+            times = []
+            for _ in range(reps):
+                wl.k_ring.copy_(snap[0])
+                wl.v_ring.copy_(snap[1])
+                pos[0].copy_(wl.pos0)
+                torch.cuda.synchronize()
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                g.replay()
+                e1.record()
+                torch.cuda.synchronize()
+                times.append(e0.elapsed_time(e1) * 1e3 / steps)
+            key = f"{'pbb_b2048' if cfg.mode == 'pbb' else 'swa_w4096'}_batch{batch}"
+            res[key] = {"us_per_step": statistics.median(times),
+                        "workspace_bytes": 0 if wl.ws is None else wl.ws.numel()}
+            del g, wl, snap
+            torch.cuda.empty_cache()
+    return res
 
 
 PAPER_ORIGINS = (8192, 16384, 32768, 65536, 131072, 262144, 524288, 1048576)
@@ -567,6 +613,7 @@ def main(argv=None):
         torch.cuda.empty_cache()
         extra["paper_shape_latency_us_per_step"] = paper_latency(
             device, shapes=(10, 12, 14), origins=(8192, 1048576))
+        extra["small_batch_latency_us_per_step"] = small_batch_latency(device)
         extra["prefill"] = prefill_extras(device)
         extra["backward"] = backward_extras(device)
         copy_gbps = copy_ceiling(device)
