@@ -29,9 +29,11 @@
 namespace pbb {
 namespace {
 
-// Waves per workgroup and 16-column groups per wave (d = 128, d = 64).
+// Waves per workgroup, 16-column groups per wave and LDS stages (d = 128, d = 64).
 constexpr int kPrefillWaves128 = 4;
 constexpr int kPrefillWaves64 = 4;
+constexpr int kPrefillStages128 = 3;
+constexpr int kPrefillStages64 = 3;
 constexpr int kPrefillColGroups128 = 2;
 constexpr int kPrefillColGroups64 = 2;
 
@@ -41,7 +43,7 @@ __device__ __forceinline__ int support_lo(const PrefillArgs& a, int t) {
 
 // Three waves per SIMD (three workgroups of 48 KiB LDS per CU): the register budget this sets
 // at d = 128 (168) leaves a few values of the epilogue in scratch, outside the key loop.
-template <int D, int QC, int NW>
+template <int D, int QC, int NW, int ST>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(3)))
 void prefill_bf16_kernel(PrefillArgs a, int tq, int tiles) {
   constexpr int KK = D / 32;            // 32-channel slices of the score contraction
@@ -53,7 +55,8 @@ void prefill_bf16_kernel(PrefillArgs a, int tq, int tiles) {
   constexpr int KTILE = 32 * ROWB;
   constexpr int VTILE = 32 * ROWB;
   constexpr int BUF = KTILE + VTILE;
-  constexpr int STAGES = 3;
+  constexpr int STAGES = ST;
+  static_assert(STAGES >= 3 && STAGES <= 5, "stages");
   constexpr int OPS = 2 * NG;           // DMA instructions per step (K tile, then V tile)
   constexpr int MYOPS = OPS / NW;       // issued by each wave
   static_assert(OPS % NW == 0, "DMA split");
@@ -175,20 +178,27 @@ void prefill_bf16_kernel(PrefillArgs a, int tq, int tiles) {
     for (int nb = 0; nb < NB; ++nb) acc[qc][nb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
   }
 
-  issue(0, 0);
-  if (nsteps > 1) issue(1, 1);
+  // Steps 0 .. STAGES-2 go out first; step st then issues step st + STAGES - 1.
+#pragma unroll
+  for (int s = 0; s < STAGES - 1; ++s)
+    if (s < nsteps) issue(s, s);
   int rstage = 0;
+  constexpr int W1 = 0x0F70 | (MYOPS & 15) | ((MYOPS >> 4) << 14);
+  constexpr int W2 = 0x0F70 | ((2 * MYOPS) & 15) | (((2 * MYOPS) >> 4) << 14);
+  constexpr int W3 = 0x0F70 | ((3 * MYOPS) & 15) | (((3 * MYOPS) >> 4) << 14);
 
   auto step = [&](int st, auto masked) {
-    // This wave's loads of step st have landed once at most step st+1's are outstanding; the
-    // barrier then covers every wave's loads, and every wave is done with step st-1, whose
-    // stage the loads of step st+2 reuse.
-    if (st + 1 < nsteps)
-      __builtin_amdgcn_s_waitcnt(0x0F70 | (MYOPS & 15) | ((MYOPS >> 4) << 14));
-    else
-      __builtin_amdgcn_s_waitcnt(0x0F70);
+    // This wave's loads of step st have landed once at most the loads of the steps issued
+    // after it (up to STAGES - 2) are outstanding; the barrier then covers every wave's loads,
+    // and every wave is done with step st-1, whose stage the loads of step st+STAGES-1 reuse.
+    const int ahead = min(STAGES - 2, nsteps - 1 - st);
+    if (ahead >= 3) __builtin_amdgcn_s_waitcnt(W3);
+    else if (ahead == 2) __builtin_amdgcn_s_waitcnt(W2);
+    else if (ahead == 1) __builtin_amdgcn_s_waitcnt(W1);
+    else __builtin_amdgcn_s_waitcnt(0x0F70);
     lds_barrier();
-    if (st + 2 < nsteps) issue(rstage == 0 ? 2 : rstage - 1, st + 2);
+    if (st + STAGES - 1 < nsteps)
+      issue(rstage == 0 ? STAGES - 1 : rstage - 1, st + STAGES - 1);
     __builtin_amdgcn_sched_barrier(0);
 
     const uint32_t sb = (uint32_t)(rstage * BUF);
@@ -358,12 +368,13 @@ template <int D>
 hipError_t launch_prefill_d(const PrefillArgs& a, hipStream_t stream) {
   constexpr int QC = D == 128 ? kPrefillColGroups128 : kPrefillColGroups64;
   constexpr int NW = D == 128 ? kPrefillWaves128 : kPrefillWaves64;
+  constexpr int ST = D == 128 ? kPrefillStages128 : kPrefillStages64;
   const int tq = 16 * QC * NW / a.group;
   const int tiles = (a.n + tq - 1) / tq;
   const size_t blocks = (size_t)a.batch * a.hkv * tiles;
   if (blocks == 0) return hipSuccess;
   if (blocks > 0x7fffffffull) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((prefill_bf16_kernel<D, QC, NW>), dim3((unsigned)blocks),
+  hipLaunchKernelGGL((prefill_bf16_kernel<D, QC, NW, ST>), dim3((unsigned)blocks),
                      dim3(NW * 64), 0, stream, a, tq, tiles);
   return hipGetLastError();
 }
