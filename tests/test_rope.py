@@ -121,3 +121,13 @@ def test_rope_graph_replay_matches_eager(cuda):
         assert torch.equal(run.k_ring.view(torch.int16), ref_k.view(torch.int16)), rep
         assert torch.equal(run.v_ring.view(torch.int16), ref_v.view(torch.int16)), rep
         _ = (qs[0].float() * 2).sum().item()
+
+
+def test_rope_split_launch(cuda):
+    """Rotary decode in a split launch (one sequence at c3's head shapes: each unit over four
+    workgroups): the workgroup that owns the current token's step patches the turned key, the
+    first workgroup appends it."""
+    cfg = _cfg("pbb", 1, 32, 8, 128, 2048, pos_hi=1 << 20, steps=5, prefill=True)
+    desc = P.make_desc(1, 32, 8, 128, block=2048, dtype=torch.bfloat16, rope_base=1e6)
+    assert P.workspace_bytes(desc) > 0
+    _run_and_check(cfg, cuda)
