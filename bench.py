@@ -453,11 +453,42 @@ def copy_ceiling(device, reps=5):
     return gbps
 
 
+def oracle_all_steps(cfg, device, threads=None):
+    """Time the fp64 CPU oracle over every step of a lockstep workload (all sequences at
+    positions 0, 1, .., steps-1; the whole history handed over once, as the oracle reads only
+    each step's support)."""
+    import numpy as np
+    import torch
+    import oracle
+    import workloads as W
+    if threads is None:
+        threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or (os.cpu_count() or 1)
+    n, T = cfg.batch, cfg.steps
+    rows = torch.arange(n, dtype=torch.int64)
+    posm = torch.arange(T, dtype=torch.int64).view(1, -1).expand(n, T)
+    kh = W.kv_at(cfg, "k", rows, posm, device=device).float().cpu().numpy()
+    vh = W.kv_at(cfg, "v", rows, posm, device=device).float().cpu().numpy()
+    qs = W.q_steps(cfg, torch.zeros(n, dtype=torch.int64), 0, T, device=device).float().cpu().numpy()
+    lo = np.zeros(n, dtype=np.int64)
+    mode = oracle.SWA if cfg.mode == "swa" else oracle.PBB
+    w0 = time.perf_counter()
+    for t in range(T):
+        oracle.decode(mode, np.full(n, t, dtype=np.int64), qs[t], kh, vh, lo, block=cfg.block,
+                      window=cfg.window, n_threads=threads)
+    el = time.perf_counter() - w0
+    return {"value": n * T / el, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"all {T} steps of {cfg.name} ({n} sequences in lockstep from position 0) "
+                      f"in {el:.1f} s; fp64 C oracle, {threads} threads"}
+
+
 def oracle_timing(device):
-    """The fp64 CPU oracle on full batches: the first decode step of every sequence of c3, c4
-    and c5, three times each with all host threads, and once single-threaded (c3)."""
+    """The fp64 CPU oracle: every step of c1 and c2, and on full batches the first decode step
+    of every sequence of c3, c4 and c5, three times each with all host threads, and once
+    single-threaded (c3)."""
     import workloads as W
     res = {"host_threads": os.cpu_count()}
+    for name in ("c1", "c2"):
+        res[name] = oracle_all_steps(W.get_config(name), device)
     for name in ("c3", "c4", "c5"):
         cfg = W.get_config(name)
         t0 = W.initial_positions(cfg)
@@ -484,7 +515,7 @@ def main(argv=None):
     ap.add_argument("--backward", action="store_true",
                     help="only run the training-backward measurements (same shapes as prefill)")
     ap.add_argument("--oracle-timing", action="store_true",
-                    help="only time the CPU oracle on full batches of c3, c4, c5 (minutes)")
+                    help="only time the CPU oracle (all steps of c1, c2; full batches of c3, c4, c5; minutes)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only time a plain 1 GiB device copy (HBM counter calibration)")
     args = ap.parse_args(argv)
