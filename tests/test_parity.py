@@ -265,3 +265,44 @@ def test_split_workgroups_small_batch(cuda, mode, batch, d, hq, hkv, block, wind
     # the launches left every unit counter at zero
     units = batch * hkv
     assert not run.ws[: 4 * units].any().item()
+
+
+@pytest.mark.parametrize("mode,dtype,d,hq,hkv,block,window,slots,rope", [
+    ("pbb", "bf16", 128, 32, 8, 2048, 0, 2048, 0.0),    # 32 units: a split launch
+    ("pbb", "f32", 64, 4, 1, 64, 0, 64, 0.0),
+    ("swa", "bf16", 128, 8, 2, 0, 4096, 4096, 0.0),
+    ("pbb", "bf16", 64, 12, 2, 128, 0, 128, 1e6),
+])
+def test_positions_at_int32_limit(cuda, mode, dtype, d, hq, hkv, block, window, slots, rope):
+    """Positions up to 2^31 - 2, the largest the boundary admits: the last block before 2^31
+    entered, bridged and left, every output against the oracle and the rings bit for bit."""
+    steps = 4
+    top = (1 << 31) - 2                      # last admissible position
+    B = block if mode == "pbb" else slots
+    t0 = torch.tensor([top - steps + 1,      # ends on the last admissible position
+                       (1 << 31) - B - 1,    # crosses into the final block
+                       (1 << 31) - B + 5,    # inside the bridge of the final block
+                       (1 << 31) - B // 2 - 2],  # leaves the bridge (r crosses h)
+                      dtype=torch.int64)
+    assert int(t0.max()) + steps - 1 <= top
+    cfg = W.Config(f"int32-limit-{mode}-{dtype}-{d}", mode, batch=4, hq=hq, hkv=hkv, d=d,
+                   block=block, slots=slots, window=window, dtype=dtype, seed=23,
+                   value_scale=1.0, pos_hi=0, steps=steps, prefill=True, rope_base=rope)
+    print(f"[int32-limit] {cfg.name}", flush=True)
+    run = Run(cfg, t0, steps, cuda)
+    rows = np.arange(4)
+    hist = run.history(rows, steps - 1)
+    for i in range(steps):
+        q, out = run.step()
+        compare(cfg, to_np(out), run.oracle_out(rows, i, q, hist=hist), what=f"{cfg.name} step {i}")
+    assert np.array_equal(run.ring_rows(rows, "v"), run.expected_ring(rows, steps - 1, "v", hist=hist))
+    if not rope:
+        assert np.array_equal(run.ring_rows(rows, "k"),
+                              run.expected_ring(rows, steps - 1, "k", hist=hist))
+    else:
+        # rotated keys: within one bf16 rounding of their exact rotation
+        exact = run.expected_rotated_keys(rows, steps - 1, hist=hist)
+        got = run.ring_rows(rows, "k").view(np.uint16).astype(np.uint32) << 16
+        err = np.abs(got.view(np.float32).astype(np.float64) - exact)
+        assert (err <= np.abs(exact) * 2.0 ** -8 + 1e-6).all()
+    assert int(run.pos.max()) == top + 1
