@@ -103,6 +103,7 @@ __device__ __forceinline__ void dma16(const unsigned char* base, uint32_t off, u
 // that takes the results as operands, so that nothing reads them earlier.
 template <int OFF>
 __device__ __forceinline__ u32x2 tr_read(uint32_t addr) {
+  static_assert(OFF >= 0 && OFF < 65536, "LDS offset immediate");
   u32x2 r;
   asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(OFF));
   return r;

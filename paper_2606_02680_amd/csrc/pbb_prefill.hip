@@ -37,6 +37,9 @@ constexpr int kPrefillStages64 = 3;
 constexpr int kPrefillColGroups128 = 2;
 constexpr int kPrefillColGroups64 = 2;
 
+// Starting reference of the running maximum (log2 units): finite and below any score.
+constexpr float kNoScore = -1.0e30f;
+
 __device__ __forceinline__ int support_lo(const PrefillArgs& a, int t) {
   return support_start(a.mode, a.block, a.window, t);
 }
@@ -168,11 +171,13 @@ void prefill_bf16_kernel(PrefillArgs a, int tq, int tiles) {
     }
   };
 
+  // m starts at a finite floor below any score, so that a column whose keys are all masked so
+  // far gets exp2(-inf - m) = 0 without a separate test; its first real maximum always moves m.
   float m[QC], lsum[QC];
   f32x4 acc[QC][NB];
 #pragma unroll
   for (int qc = 0; qc < QC; ++qc) {
-    m[qc] = kNegInf;
+    m[qc] = kNoScore;
     lsum[qc] = 0.0f;
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) acc[qc][nb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
@@ -224,13 +229,15 @@ void prefill_bf16_kernel(PrefillArgs a, int tq, int tiles) {
     // accumulators are rescaled) when some column's maximum exceeds it by more than 8, so that
     // most steps skip the rescale and the weights stay <= 2^8.  The result is the same softmax:
     // numerator and denominator share every reference change.
+    // A column's maximum exceeds m + 8 only if the maximum of one of its four lanes does, so
+    // the cross-lane reduction runs only in steps where some lane's own maximum does.
     const float c = a.scale_log2;
     bf16x8 pB[QC];
-    float alpha[QC];
-    bool grow_any = false;
+    float mx[QC];
+    bool over = false;
 #pragma unroll
     for (int qc = 0; qc < QC; ++qc) {
-      float mx = kNegInf;
+      mx[qc] = kNegInf;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         float sc = e < 4 ? s0[qc][e] : s1[qc][e - 4];
@@ -239,31 +246,37 @@ void prefill_bf16_kernel(PrefillArgs a, int tq, int tiles) {
           sc = (key >= lo_c[qc] && key <= hi_c[qc]) ? sc : kNegInf;
           if (e < 4) s0[qc][e] = sc; else s1[qc][e - 4] = sc;
         }
-        mx = fmaxf(mx, sc);
+        mx[qc] = fmaxf(mx[qc], sc);
       }
-      mx = max_xor16_32(mx);
-      const float cand = mx * c;
-      const bool grow = cand > m[qc] + 8.0f;
-      alpha[qc] = grow ? fast_exp2(m[qc] - cand) : 1.0f;
-      m[qc] = grow ? cand : m[qc];
-      grow_any |= grow;
+      over |= mx[qc] * c > m[qc] + 8.0f;
     }
-    if (__builtin_amdgcn_ballot_w64(grow_any) != 0) {
+    if (__builtin_amdgcn_ballot_w64(over) != 0) {
+      float alpha[QC];
+      bool grow_any = false;
 #pragma unroll
       for (int qc = 0; qc < QC; ++qc) {
-        lsum[qc] *= alpha[qc];
+        const float cand = max_xor16_32(mx[qc]) * c;
+        const bool grow = cand > m[qc] + 8.0f;
+        alpha[qc] = grow ? fast_exp2(m[qc] - cand) : 1.0f;
+        m[qc] = grow ? cand : m[qc];
+        grow_any |= grow;
+      }
+      if (__builtin_amdgcn_ballot_w64(grow_any) != 0) {
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) acc[qc][nb] *= alpha[qc];
+        for (int qc = 0; qc < QC; ++qc) {
+          lsum[qc] *= alpha[qc];
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb) acc[qc][nb] *= alpha[qc];
+        }
       }
     }
 #pragma unroll
     for (int qc = 0; qc < QC; ++qc) {
-      const float ms = m[qc] == kNegInf ? 0.0f : m[qc];  // a column with no key yet stays empty
       float ps = 0.0f;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const float sc = e < 4 ? s0[qc][e] : s1[qc][e - 4];
-        const float pe = fast_exp2(__builtin_fmaf(sc, c, -ms));
+        const float pe = fast_exp2(__builtin_fmaf(sc, c, -m[qc]));
         ps += pe;
         pB[qc][e] = (__bf16)pe;
       }
