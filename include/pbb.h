@@ -226,7 +226,7 @@ pbb_status_t swa_prefill(const pbb_desc_t *desc, int32_t n, const void *q, const
  * (PBB_ERR_SHAPE otherwise).  Alignment as pbb_prefill.
  * workspace: device memory of pbb_backward_workspace_bytes bytes = 8 * batch * n_q_heads * n
  * rounded up to a multiple of 256 (16-byte aligned, contents irrelevant; holds lse * log2(e)
- * and delta per position); PBB_ERR_WORKSPACE if NULL or smaller.  Enqueues two kernels on
+ * and -delta per position); PBB_ERR_WORKSPACE if NULL or smaller.  Enqueues two kernels on
  * the stream.  The gradient buffers must not alias the inputs.
  */
 pbb_status_t pbb_backward_workspace_bytes(const pbb_desc_t *desc, int32_t n, size_t *bytes);

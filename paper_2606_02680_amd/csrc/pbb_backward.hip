@@ -11,7 +11,8 @@
 //   dq:    the prefill kernel's structure (128 query columns per workgroup, two 16-column
 //          groups per wave, walk their key interval in 32-key steps through LDS), no running
 //          maximum (lse is known); each column also computes its delta and lse * log2(e) and
-//          writes them to the workspace for the second launch;
+//          writes lse * log2(e) and -delta to the workspace for the second launch (both
+//          launches start the dout.v accumulators at -delta, so the MFMA yields dp - delta);
 //   dk/dv: transposed roles: each workgroup holds 64 keys of one KV head in registers and
 //          walks, for every query head of the group, the interval of targets whose supports
 //          contain those keys (PBB: up to h(floor(s/h) + 2) - 1; SWA: s + W - 1).
@@ -95,7 +96,7 @@ void bwd_dq_kernel(BackwardArgs a, int tq, int tiles) {
   // This lane's query columns: column c -> position t0 + c / G, head g*G + c % G.
   int tc[QC], hc[QC], lo_c[QC], hi_c[QC];
   bool valid[QC];
-  float lse2[QC], dlt[QC];
+  float lse2[QC], ndl[QC];  // lse * log2(e) and -delta of each column
   bf16x8 qB[QC][KK], gB[QC][KK], oB[QC][KK];
 #pragma unroll
   for (int qc = 0; qc < QC; ++qc) {
@@ -179,8 +180,8 @@ void bwd_dq_kernel(BackwardArgs a, int tq, int tiles) {
   int rstage = 0;
 
   // delta = dout . out of each column (the four quarters j hold channel slices 8j.. of every
-  // 32-channel block), and lse * log2(e): kept in registers for dq and written to the workspace
-  // for the dk/dv launch.
+  // 32-channel block), and lse * log2(e): -delta and lse * log2(e) are kept in registers for dq
+  // and written to the workspace for the dk/dv launch.
 #pragma unroll
   for (int qc = 0; qc < QC; ++qc) {
     float part = 0.0f;
@@ -189,11 +190,11 @@ void bwd_dq_kernel(BackwardArgs a, int tq, int tiles) {
 #pragma unroll
       for (int e = 0; e < 8; ++e)
         part = __builtin_fmaf((float)gB[qc][kk][e], (float)oB[qc][kk][e], part);
-    dlt[qc] = sum_xor16_32(part);
+    ndl[qc] = -sum_xor16_32(part);
     if (valid[qc] && j4 == 0) {
       float* w = a.ws + ((size_t)b * a.hq + hc[qc]) * 2 * n + tc[qc];
       w[0] = lse2[qc];
-      w[n] = dlt[qc];
+      w[n] = ndl[qc];
     }
   }
 
@@ -212,8 +213,8 @@ void bwd_dq_kernel(BackwardArgs a, int tq, int tiles) {
     for (int qc = 0; qc < QC; ++qc) {
       s0[qc] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
       s1[qc] = s0[qc];
-      d0[qc] = s0[qc];
-      d1[qc] = s0[qc];
+      d0[qc] = f32x4{ndl[qc], ndl[qc], ndl[qc], ndl[qc]};  // the products land on -delta
+      d1[qc] = d0[qc];
     }
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
@@ -237,7 +238,8 @@ void bwd_dq_kernel(BackwardArgs a, int tq, int tiles) {
       kr[2 * nb] = tr_read<0>(kaddr[nb] + sb);
       kr[2 * nb + 1] = tr_read<16 * ROWB>(kaddr[nb] + sb);
     }
-    // ds = p (dp - delta), p = exp2(s c - lse2); masked keys give p = 0.
+    // ds = p (dp - delta) (the accumulators started at -delta), p = exp2(s c - lse2); masked
+    // keys give p = 0.
     bf16x8 dsB[QC];
 #pragma unroll
     for (int qc = 0; qc < QC; ++qc) {
@@ -250,7 +252,7 @@ void bwd_dq_kernel(BackwardArgs a, int tq, int tiles) {
           const int key = k0 + (e < 4 ? 4 * j4 + e : 16 + 4 * j4 + (e - 4));
           pe = (key >= lo_c[qc] && key <= hi_c[qc]) ? pe : 0.0f;
         }
-        dsB[qc][e] = (__bf16)(pe * (dp - dlt[qc]));
+        dsB[qc][e] = (__bf16)(pe * dp);
       }
     }
     // dq^T += K^T ds^T.
@@ -306,14 +308,14 @@ void bwd_dq_kernel(BackwardArgs a, int tq, int tiles) {
 // matrix-core B operands, sharing every Q and dout read of a step); the workgroup walks, for
 // each query head of the group in turn, the 32-target steps of the targets whose supports
 // contain its keys, through LDS: Q and dout rows (dual layout) and the steps' lse * log2(e)
-// and delta values.
+// and -delta values.
 template <int D, int NW, int KC, int WPE>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(WPE)))
 void bwd_dkdv_kernel(BackwardArgs a, int tiles) {
   constexpr int KK = D / 32, NB = D / 16, ROWB = D * 2, PPR = D / 8, RPI = 64 / PPR;
   constexpr int NG = 32 / RPI;
   constexpr int TILE = 32 * ROWB;
-  constexpr int BUF = 2 * TILE + 256;   // Q tile, dout tile, lse2[32] and delta[32]
+  constexpr int BUF = 2 * TILE + 256;   // Q tile, dout tile, lse2[32] and -delta[32]
   constexpr int STAGES = 3;
   constexpr int ROWOPS = 2 * NG;        // row DMAs per step; wave 0 also issues the lse/delta one
   constexpr int MYOPS = ROWOPS / NW;
@@ -369,7 +371,7 @@ void bwd_dkdv_kernel(BackwardArgs a, int tiles) {
 
   // DMA of (head hi, target step j): rows q0 .. q0+31 of Q and dout (wave-uniform base, lane
   // offset row * qrowstride + piece; rows past q_end read the last piece of row q_end), and,
-  // from wave 0, lse2 (lanes 0..31) and delta (lanes 32..63) of the same targets.
+  // from wave 0, lse2 (lanes 0..31) and -delta (lanes 32..63) of the same targets.
   const uint32_t qrowstride = (uint32_t)a.hq * ROWB;
   const unsigned char* qb0 = (const unsigned char*)a.q + ((size_t)b * n * a.hq + g * G) * ROWB;
   const unsigned char* gb0 = (const unsigned char*)a.dout + ((size_t)b * n * a.hq + g * G) * ROWB;
@@ -468,14 +470,21 @@ void bwd_dkdv_kernel(BackwardArgs a, int tiles) {
     __builtin_amdgcn_sched_barrier(0);
     const uint32_t sb = (uint32_t)(rstage * BUF);
     const int q0 = q_first + 32 * j;
-    // Scores with targets on the rows (two halves of 16) and this wave's keys on the columns.
+    // lse2 and -delta of this lane's 8 targets (rows 4j..4j+3 and 16+4j..16+4j+3).
+    const auto* lp = lds0 + lbase + sb + 16 * j4;
+    const f32x4 la = *(const __attribute__((address_space(3))) f32x4*)(lp);
+    const f32x4 lb = *(const __attribute__((address_space(3))) f32x4*)(lp + 64);
+    const f32x4 da = *(const __attribute__((address_space(3))) f32x4*)(lp + 128);
+    const f32x4 db = *(const __attribute__((address_space(3))) f32x4*)(lp + 192);
+    // Scores with targets on the rows (two halves of 16) and this wave's keys on the columns;
+    // the dout.v products land on -delta of their target row.
     f32x4 s0[KC], s1[KC], d0[KC], d1[KC];
 #pragma unroll
     for (int kc = 0; kc < KC; ++kc) {
       s0[kc] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
       s1[kc] = s0[kc];
-      d0[kc] = s0[kc];
-      d1[kc] = s0[kc];
+      d0[kc] = da;
+      d1[kc] = db;
     }
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
@@ -492,12 +501,6 @@ void bwd_dkdv_kernel(BackwardArgs a, int tiles) {
         d1[kc] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gb, vB[kc][kk], d1[kc], 0, 0, 0);
       }
     }
-    // lse2 and delta of this lane's 8 targets (rows 4j..4j+3 and 16+4j..16+4j+3).
-    const auto* lp = lds0 + lbase + sb + 16 * j4;
-    const f32x4 la = *(const __attribute__((address_space(3))) f32x4*)(lp);
-    const f32x4 lb = *(const __attribute__((address_space(3))) f32x4*)(lp + 64);
-    const f32x4 da = *(const __attribute__((address_space(3))) f32x4*)(lp + 128);
-    const f32x4 db = *(const __attribute__((address_space(3))) f32x4*)(lp + 192);
     // The dout^T reads for dv go out now, under the softmax arithmetic.
     u32x2 gr[2 * NB];
 #pragma unroll
@@ -513,14 +516,13 @@ void bwd_dkdv_kernel(BackwardArgs a, int tiles) {
         const float sc = e < 4 ? s0[kc][e] : s1[kc][e - 4];
         const float dp = e < 4 ? d0[kc][e] : d1[kc][e - 4];
         const float l2 = e < 4 ? la[e] : lb[e - 4];
-        const float dl = e < 4 ? da[e] : db[e - 4];
         float pe = fast_exp2(__builtin_fmaf(sc, c, -l2));
         if constexpr (decltype(masked)::value) {
           const int t = q0 + (e < 4 ? 4 * j4 + e : 16 + 4 * j4 + (e - 4));
           pe = (t >= t_lo[kc] && t <= t_hi[kc]) ? pe : 0.0f;
         }
         pB[kc][e] = (__bf16)pe;
-        dsB[kc][e] = (__bf16)(pe * (dp - dl));
+        dsB[kc][e] = (__bf16)(pe * dp);
       }
     }
     // dv^T += dout^T p, dk^T += Q^T ds: dout^T and Q^T by transposed reads.
