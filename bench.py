@@ -483,8 +483,8 @@ def oracle_all_steps(cfg, device, threads=None):
 
 def oracle_timing(device):
     """The fp64 CPU oracle: every step of c1 and c2, and on full batches the first decode step
-    of every sequence of c3, c4 and c5, three times each with all host threads, and once
-    single-threaded (c3)."""
+    of every sequence of c3, c4 and c5, at least three times and 5 s each with all host
+    threads, and once single-threaded (c3)."""
     import workloads as W
     res = {"host_threads": os.cpu_count()}
     for name in ("c1", "c2"):
@@ -492,7 +492,7 @@ def oracle_timing(device):
     for name in ("c3", "c4", "c5"):
         cfg = W.get_config(name)
         t0 = W.initial_positions(cfg)
-        res[name] = cpu_baseline(cfg, t0, device, budget_s=0.0, n_seq=cfg.batch, min_reps=3)
+        res[name] = cpu_baseline(cfg, t0, device, budget_s=5.0, n_seq=cfg.batch, min_reps=3)
     cfg = W.get_config("c3")
     res["c3_single_thread"] = cpu_baseline(cfg, W.initial_positions(cfg), device, budget_s=0.0,
                                            n_seq=cfg.batch, min_reps=1, threads=1)
