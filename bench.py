@@ -609,7 +609,11 @@ def main(argv=None):
         inputs = wl.inputs
         del wl
         torch.cuda.empty_cache()
+        # SWA rings on the same tensors: the graded W = 2B window, and the paper's own
+        # comparison window W = B in a buffer of 2B slots and in a ring of B slots.
         for name, c in (("swa_ring_w4096_s4096", W.get_config("c5")),
+                        ("swa_ring_w2048_s4096", W.get_config("c5").with_(window=2048,
+                                                                          slots=4096)),
                         ("swa_ring_w2048_s2048", W.get_config("c5").with_(window=2048,
                                                                           slots=2048))):
             sw = Workload(c, t0, n_steps, device, inputs=inputs)
