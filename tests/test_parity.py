@@ -306,3 +306,31 @@ def test_positions_at_int32_limit(cuda, mode, dtype, d, hq, hkv, block, window, 
         err = np.abs(got.view(np.float32).astype(np.float64) - exact)
         assert (err <= np.abs(exact) * 2.0 ** -8 + 1e-6).all()
     assert int(run.pos.max()) == top + 1
+
+
+@pytest.mark.parametrize("mode,dtype,hq,hkv,B", [
+    ("pbb", "bf16", 8, 1, 65536),   # one unit: a split launch over the longest supports
+    ("pbb", "f32", 4, 1, 65536),
+    ("swa", "bf16", 4, 2, 65536),
+])
+def test_largest_ring(cuda, mode, dtype, hq, hkv, B):
+    """Rings of the largest admitted size (65536 slots) with supports of up to 65536 keys:
+    the bridge at its longest (phase h - 1 after a full block), a block's first phase, its
+    last phase, and an SWA window of 65536."""
+    h = B // 2
+    t0 = torch.tensor([B + h - 2, 2 * B, 2 * B - 1], dtype=torch.int64)  # phases h-2.., 0.., B-1..
+    steps = 2
+    window = B if mode == "swa" else 0
+    cfg = W.Config(f"largest-ring-{mode}-{dtype}", mode, batch=3, hq=hq, hkv=hkv, d=64,
+                   block=B if mode == "pbb" else 0, slots=B, window=window, dtype=dtype,
+                   seed=29, value_scale=1.0, pos_hi=0, steps=steps, prefill=True)
+    print(f"[largest-ring] {cfg.name}", flush=True)
+    run = Run(cfg, t0, steps, cuda)
+    rows = np.arange(3)
+    hist = run.history(rows, steps - 1)
+    for i in range(steps):
+        q, out = run.step()
+        compare(cfg, to_np(out), run.oracle_out(rows, i, q, hist=hist), what=f"{cfg.name} step {i}")
+    for which in ("k", "v"):
+        assert np.array_equal(run.ring_rows(rows, which),
+                              run.expected_ring(rows, steps - 1, which, hist=hist)), which
