@@ -175,3 +175,44 @@ def test_prefill_bench_shapes(cuda, name, shape):
             compare(cfg, got, ref[:, first:], what=f"{name} seq {b} group {g} [{a0 + first}, {a1})")
             gl = lse[b:b + 1, hs, a0 + first:a1].cpu().numpy().astype(np.float64)
             assert np.abs(gl - ref_lse[:, :, first:]).max() <= 2e-3
+
+
+@pytest.mark.parametrize("mode,hq,hkv,block,window", [
+    ("pbb", 16, 1, 65536, 0),     # group of 16, supports up to 65536 keys
+    ("swa", 4, 2, 0, 65536),
+])
+def test_prefill_largest_ring_sampled(cuda, mode, hq, hkv, block, window):
+    """A 70000-position prompt with the largest admitted block or window (65536): outputs and
+    log-partitions of sampled positions (block and bridge edges, the longest supports, the
+    last position) against the decode oracle at each position over the prompt's history, and
+    the ring state bit for bit."""
+    n = 70000
+    cfg = _cfg(mode, 1, n, hq, hkv, 64, block=block, window=window)
+    desc, (q, k, v), out, lse, kr, vr = _run(cfg, n, cuda)
+    B = block or window
+    h = B // 2
+    picks = {0, 1, 31, 32, h - 1, h, h + 1, B - 1, B, B + 1, B + h - 2, B + h - 1, B + h,
+             n - 2, n - 1} | set(np.random.default_rng(5).integers(0, n, 24).tolist())
+    t = np.array(sorted(p for p in picks if 0 <= p < n), dtype=np.int64)
+    assert t.min() >= 0 and t.max() < n   # indices into the prompt, checked on the host
+    kh = to_np(k[0].permute(1, 0, 2).contiguous())[None]   # [1][Hkv][n][d]
+    vh = to_np(v[0].permute(1, 0, 2).contiguous())[None]
+    m = oracle.SWA if mode == "swa" else oracle.PBB
+    qs = to_np(q[0, torch.as_tensor(t, device=cuda)])     # [len(t)][Hq][d]
+    ref = np.stack([oracle.decode(m, np.array([tt]), qs[i:i + 1], kh, vh, np.zeros(1, np.int64),
+                                  block=block, window=window)[0] for i, tt in enumerate(t)])
+    got = to_np(out[0, torch.as_tensor(t, device=cuda)])
+    compare(cfg, got, ref, what=f"{cfg.name} sampled positions")
+    # log-partitions: the dense masked softmax of each sampled position, in fp64
+    scale = 1.0 / np.sqrt(64.0)
+    G = hq // hkv
+    for i, tt in enumerate(t):
+        lo = max(0, h * (tt // h - 1)) if mode == "pbb" else max(0, tt - window + 1)
+        for hd in range(hq):
+            z = kh[0, hd // G, lo:tt + 1].astype(np.float64) @ qs[i, hd].astype(np.float64) * scale
+            ref_lse = z.max() + np.log(np.exp(z - z.max()).sum())
+            assert abs(float(lse[0, hd, tt]) - ref_lse) <= 2e-3, (tt, hd)
+    # ring: slot s mod slots holds the last prompt position s
+    kb = bits(kr[0])
+    for s in (n - 1, n - 2, n - B if n - B >= 0 else 0, n - 40000):
+        assert np.array_equal(kb[:, s % desc.slots], bits(k[0, s]).reshape(hkv, -1)), s
