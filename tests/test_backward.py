@@ -155,3 +155,45 @@ def test_backward_bench_shapes(cuda, name, shape):
             _grad_ok(f"{name} dq seq {b} group {g} [{a0}, {a1})", sl(dq, hs), rq)
             _grad_ok(f"{name} dk seq {b} group {g} [{a0}, {a1})", sl(dk, slice(g, g + 1)), rk)
             _grad_ok(f"{name} dv seq {b} group {g} [{a0}, {a1})", sl(dv, slice(g, g + 1)), rv)
+
+
+@pytest.mark.parametrize("mode,hq,hkv,block,window", [
+    ("pbb", 16, 1, 65536, 0),
+    ("swa", 4, 2, 0, 65536),
+])
+def test_backward_largest_ring(cuda, mode, hq, hkv, block, window):
+    """A 70000-position prompt with the largest block or window (65536), so that dk/dv
+    workgroups of the first keys walk ~65536 targets for each of up to 16 heads.  The upstream
+    gradient is nonzero on the prefix [0, 1024) only: there the gradients match the oracle on
+    the prefix (whose supports lie inside it), and every other row is exactly zero."""
+    n, npre, d = 70000, 1024, 64
+    G = hq // hkv
+    cfg = W.Config(f"bwd-largest-{mode}", mode, batch=1, hq=hq, hkv=hkv, d=d, block=block,
+                   slots=block or window, window=window, dtype="bf16", seed=17, value_scale=1.0,
+                   pos_hi=0, steps=1)
+    q, k, v = W.prompt(cfg, n, device=cuda)
+    dfull, _, _ = W.prompt(cfg.with_(seed=18), n, device=cuda)
+    keep = torch.zeros(n, dtype=dfull.dtype, device=cuda)
+    keep[:npre] = 1
+    dout = (dfull * keep.view(1, n, 1, 1)).contiguous()
+    if mode == "pbb":
+        desc = P.make_desc(1, hq, hkv, d, block=block, dtype=torch.bfloat16)
+        fwd, bwd = P.pbb_prefill, P.pbb_backward
+    else:
+        desc = P.make_desc(1, hq, hkv, d, window=window, slots=window, dtype=torch.bfloat16)
+        fwd, bwd = P.swa_prefill, P.swa_backward
+    out = torch.empty_like(q)
+    lse = torch.empty((1, hq, n), dtype=torch.float32, device=cuda)
+    fwd(desc, q, k, v, out, lse)
+    dq, dk, dv = (torch.full_like(x, float("nan")) for x in (q, k, v))
+    print(f"[backward] largest ring {mode} n={n}", flush=True)
+    bwd(desc, q, k, v, out, dout, lse, dq, dk, dv)
+    torch.cuda.synchronize()
+    assert not dq[:, npre:].any().item()
+    assert not dk[:, npre:].any().item() and not dv[:, npre:].any().item()
+    om = oracle.SWA if mode == "swa" else oracle.PBB
+    sl = lambda x: to_np(x[:, :npre])
+    rq, rk, rv = oracle.backward(om, sl(q), sl(k), sl(v), sl(dout), block=block, window=window)
+    _grad_ok(f"largest {mode} dq", sl(dq), rq)
+    _grad_ok(f"largest {mode} dk", sl(dk), rk)
+    _grad_ok(f"largest {mode} dv", sl(dv), rv)
