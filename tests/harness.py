@@ -149,7 +149,19 @@ class Run:
         h = kh if which == "k" else vh
         t_last = self.t0.numpy()[rows] + step
         first = np.maximum(0, self.t0.numpy()[rows] - self.hist_len)
-        return oracle.expected_ring(bits(h), lo, t_last, first, self.desc.slots)
+        return oracle.expected_ring(self._bits_of(h), lo, t_last, first, self.desc.slots)
+
+    def _bits_of(self, h: torch.Tensor) -> np.ndarray:
+        """bits(h), kept for the last two history tensors (a run checked every step reuses its
+        K and V histories; copying them to the host each time would dominate)."""
+        cache = self.__dict__.setdefault("_bits_cache", [])
+        for t, val in cache:
+            if t is h:          # the cache holds h itself, so its storage cannot be reused
+                return val
+        val = bits(h)
+        cache.append((h, val))
+        del cache[:-2]
+        return val
 
     def expected_rotated_keys(self, rows: np.ndarray, step: int, hist=None) -> np.ndarray:
         """fp64 image of the K ring of a rotary run after ``step``: every slot holds the exact
