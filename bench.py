@@ -514,6 +514,9 @@ def main(argv=None):
                     help="only run the prefill measurements (c3 head shapes and paper shape)")
     ap.add_argument("--backward", action="store_true",
                     help="only run the training-backward measurements (same shapes as prefill)")
+    ap.add_argument("--small-batch", action="store_true",
+                    help="only run the small-batch latency graphs (batches 1, 4, 8, 16 at c3's "
+                         "head shapes; split launches up to 32 units)")
     ap.add_argument("--oracle-timing", action="store_true",
                     help="only time the CPU oracle (all steps of c1, c2; full batches of c3, c4, c5; minutes)")
     ap.add_argument("--copy-probe", action="store_true",
@@ -563,6 +566,11 @@ def main(argv=None):
     if args.paper_latency:
         print(json.dumps({"paper_shape_latency_us_per_step":
                           paper_latency(device, origins=PAPER_ORIGINS)}), flush=True)
+        return 0
+
+    if args.small_batch:
+        print(json.dumps({"small_batch_latency_us_per_step":
+                          small_batch_latency(device, batches=(1, 4, 8, 16))}), flush=True)
         return 0
 
     cfg = W.get_config(args.config)
