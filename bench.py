@@ -516,7 +516,7 @@ def main(argv=None):
                     help="only run the training-backward measurements (same shapes as prefill)")
     ap.add_argument("--small-batch", action="store_true",
                     help="only run the small-batch latency graphs (batches 1, 4, 8, 16 at c3's "
-                         "head shapes; split launches up to 32 units)")
+                         "head shapes; split launches up to 64 units)")
     ap.add_argument("--oracle-timing", action="store_true",
                     help="only time the CPU oracle (all steps of c1, c2; full batches of c3, c4, c5; minutes)")
     ap.add_argument("--copy-probe", action="store_true",

@@ -121,8 +121,8 @@ pbb_status_t pbb_ring_fill(const pbb_desc_t *desc, const int32_t *pos, const voi
 
 /*
  * Workspace bytes pbb_decode_step needs.  0 unless the launch is split: bf16 launches with at
- * most 32 (sequence, KV head) units and supports of at least 32 32-key steps spread each unit's
- * support over several workgroups,
+ * most 64 (sequence, KV head) units whose block (or window) exceeds 256 keys spread each unit's
+ * support over up to eight workgroups,
  * which leave partial softmax states (Eq.(lse), Appendix A.4) in the workspace for the last of
  * them to merge.  Its first 256-byte-aligned part holds one counter per unit: it must be
  * zero-filled before the first call, and every call leaves it zero again, so one allocation

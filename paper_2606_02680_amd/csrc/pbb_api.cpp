@@ -18,7 +18,8 @@ constexpr int32_t kMaxGroup = 16;     // query heads per KV head held by one MFM
 constexpr int32_t kMaxSlots = 65536;  // ring slots per (sequence, KV head)
 constexpr int32_t kMaxPrefill = 1 << 30;  // prompt positions per call
 constexpr int64_t kSplitUnits = 256;      // workgroups a split decode launch aims for (CUs)
-constexpr int64_t kSplitMaxUnits = 32;    // bf16 decode launches with at most this many units split
+constexpr int64_t kSplitMaxUnits = 64;    // bf16 decode launches with at most this many units split
+constexpr int64_t kSplitMaxWays = 8;      // workgroups per unit of a split launch, at most
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
@@ -53,16 +54,18 @@ size_t ring_tensor_bytes(const pbb_desc_t* d) {
 }
 
 // Workgroups per (sequence, KV head) unit of a bf16 decode launch: launches with few units
-// spread each unit's key steps over several workgroups (at least 16 32-key steps, four per wave
-// of a 4-wave workgroup), so that more of the chip streams the rings.  The merge through the
-// workspace costs three serial device-coherent round trips (~5 us), which only pays off for
-// small batches with long supports.
+// spread each unit's key steps over up to eight workgroups (at least eight 32-key steps each,
+// two per wave of a 4-wave workgroup), so that more of the chip streams the rings.  The merge
+// through the workspace costs a few serial device-coherent round trips (~2-3 us), which pays
+// off for small batches with long supports.
 int32_t decode_splits(const pbb_desc_t* d, bool swa) {
   if (d->dtype != PBB_DTYPE_BF16) return 1;
   const int64_t units = (int64_t)d->batch * d->n_kv_heads;
   if (units > kSplitMaxUnits) return 1;
   const int64_t max_steps = ((int64_t)(swa ? d->window : d->block) + 31) / 32;
-  const int64_t s = std::min((kSplitUnits + units - 1) / units, (max_steps + 15) / 16);
+  int64_t s = std::min((kSplitUnits + units - 1) / units, (max_steps + 7) / 8);
+  s = std::min<int64_t>(s, kSplitMaxWays);
+  s = std::min<int64_t>(s, pbb::kMaxSplitStates / (d->n_q_heads / d->n_kv_heads));
   return (int32_t)std::max<int64_t>(1, s);
 }
 

@@ -10,6 +10,10 @@ namespace pbb {
 
 enum SupportMode : int32_t { kSupportPBB = 0, kSupportSWA = 1 };
 
+// Largest number of (split, query head) states one unit of a split decode launch merges (the
+// merge stages their maxima and sums in LDS).
+constexpr int kMaxSplitStates = 2048;
+
 // Everything a decode kernel needs, validated on the host before launch.
 struct DecodeArgs {
   const int32_t* pos;

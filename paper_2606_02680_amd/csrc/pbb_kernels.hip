@@ -314,7 +314,11 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
   constexpr int OPS = 2 * NG;           // DMA instructions per step
   constexpr int STAGE_BYTES = NW * 2 * BUF;
   constexpr int MERGE_BYTES = NW * 16 * (D + 2) * 4;
-  constexpr int SMEM = STAGE_BYTES > MERGE_BYTES + 16 ? STAGE_BYTES : MERGE_BYTES + 16;
+  // Split launches merge up to kMaxSplitStates (splits x heads) states through LDS after the
+  // wave merge area and the arrival flag.
+  constexpr int SPLIT_BYTES = SPLIT ? (2 * kMaxSplitStates + 16) * 4 : 0;
+  constexpr int SMEM = STAGE_BYTES > MERGE_BYTES + 16 + SPLIT_BYTES ? STAGE_BYTES
+                                                                    : MERGE_BYTES + 16 + SPLIT_BYTES;
   __shared__ __align__(16) unsigned char smem[SMEM];
 
   const int S = SPLIT ? a.splits : 1;
@@ -678,20 +682,52 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
                                      __HIP_MEMORY_SCOPE_AGENT) == (unsigned)(S - 1) ? 1 : 0;
     __syncthreads();
     if (*last) {
+      // The S states' maxima and sums go to LDS first (all loads of a thread in flight
+      // together), one thread per head turns them into weights exp2(m_s - M) and the total
+      // L, and every output element then sums its S partial outputs, issuing several loads
+      // before waiting: a handful of serial memory round trips instead of two per split and
+      // element.
       const float* p0 = a.ws_part + (size_t)bg * S * G * (D + 2);
+      float* wm = (float*)(smem + MERGE_BYTES + 16);   // [S][G] maxima, then weights
+      float* wl = wm + S * G;                          // [S][G] sums
+      float* hl = wl + S * G;                          // [G] totals
+      for (int i = tid; i < S * G; i += NW * 64) {
+        const int sx = i / G;
+        const float* ps = p0 + (size_t)sx * G * (D + 2) + G * D + (i - sx * G);
+        const float mv = coherent_load(ps);
+        const float lv = coherent_load(ps + G);
+        wm[i] = mv;
+        wl[i] = lv;
+      }
+      __syncthreads();
+      if (tid < G) {
+        float M = kNegInf;
+        for (int sx = 0; sx < S; ++sx) M = fmaxf(M, wm[sx * G + tid]);
+        float L = 0.0f;
+        for (int sx = 0; sx < S; ++sx) {
+          const float ms = wm[sx * G + tid];
+          const float wt = (ms == kNegInf) ? 0.0f : fast_exp2(ms - M);
+          wm[sx * G + tid] = wt;
+          L += wt * wl[sx * G + tid];
+        }
+        hl[tid] = L;
+      }
+      __syncthreads();
       for (int idx = tid; idx < G * D; idx += NW * 64) {
         const int h = idx / D;
-        float M = kNegInf;
-        for (int s = 0; s < S; ++s) M = fmaxf(M, coherent_load(p0 + (size_t)s * G * (D + 2) + G * D + h));
-        float L = 0.0f, O = 0.0f;
-        for (int s = 0; s < S; ++s) {
-          const float* ps = p0 + (size_t)s * G * (D + 2);
-          const float ms = coherent_load(ps + G * D + h);
-          const float wt = (ms == kNegInf) ? 0.0f : fast_exp2(ms - M);
-          L += wt * coherent_load(ps + G * D + G + h);
-          O += wt * coherent_load(ps + idx);
+        float O = 0.0f;
+        for (int s0 = 0; s0 < S; s0 += 8) {
+          // eight loads in flight per wait; past the last split the loads repeat it (in
+          // bounds) and are not added
+          float o[8];
+#pragma unroll
+          for (int j = 0; j < 8; ++j)
+            o[j] = coherent_load(p0 + (size_t)min(s0 + j, S - 1) * G * (D + 2) + idx);
+#pragma unroll
+          for (int j = 0; j < 8; ++j)
+            if (s0 + j < S) O += wm[(s0 + j) * G + h] * o[j];
         }
-        out[idx] = float_to_bf16_rne(O / L);
+        out[idx] = float_to_bf16_rne(O / hl[h]);
       }
       if (tid == 0)
         __hip_atomic_store(&a.counters[bg], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);

@@ -250,14 +250,16 @@ def test_backward_argument_errors(fn):
 
 
 def test_split_decode_workspace():
-    """bf16 launches with at most 32 (sequence, KV head) units split each unit over several
+    """bf16 launches with at most 64 (sequence, KV head) units split each unit over up to eight
     workgroups and need a workspace: counters (256-byte aligned) plus partial states."""
     one = B.make_desc(1, 32, 8, 128, block=2048, dtype=torch.bfloat16)
-    # 8 units -> min(ceil(256 / 8), ceil(64 / 16)) = 4 workgroups per unit
-    assert P.workspace_bytes(one) == 256 + 8 * 4 * 4 * (128 + 2) * 4
+    # 8 units -> min(ceil(256 / 8), ceil(64 / 8), 8) = 8 workgroups per unit
+    assert P.workspace_bytes(one) == 256 + 8 * 8 * 4 * (128 + 2) * 4
     swa = B.make_desc(2, 8, 2, 128, window=4096, slots=4096, dtype=torch.bfloat16)
-    assert P.swa_workspace_bytes(swa) == 256 + 4 * min(64, 8) * 4 * 130 * 4
-    many = B.make_desc(5, 32, 8, 128, block=2048, dtype=torch.bfloat16)   # 40 units
+    assert P.swa_workspace_bytes(swa) == 256 + 4 * min(64, 16, 8) * 4 * 130 * 4
+    mid = B.make_desc(5, 32, 8, 128, block=2048, dtype=torch.bfloat16)    # 40 units
+    assert P.workspace_bytes(mid) == 256 + 40 * 7 * 4 * 130 * 4           # ceil(256 / 40) = 7
+    many = B.make_desc(9, 32, 8, 128, block=2048, dtype=torch.bfloat16)   # 72 units
     assert P.workspace_bytes(many) == 0
     short = B.make_desc(1, 32, 8, 128, block=256, dtype=torch.bfloat16)   # 8 steps at most
     assert P.workspace_bytes(short) == 0

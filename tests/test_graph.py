@@ -163,7 +163,7 @@ def test_advance_variant_matches_plain_steps(cuda, mode):
 
 
 def test_graph_replay_with_split_workgroups(cuda):
-    """A split launch (one sequence at c3's head shapes: each unit over 4 workgroups that merge
+    """A split launch (one sequence at c3's head shapes: each unit over 8 workgroups that merge
     through the workspace, whose counters every launch leaves at zero) captured as a 48-step
     graph with on-device position advance: every replay reproduces eager execution bit for
     bit."""

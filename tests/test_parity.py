@@ -233,10 +233,12 @@ def test_snapshot_restore_continues_bitwise(cuda):
 
 
 @pytest.mark.parametrize("mode,batch,d,hq,hkv,block,window,slots,pos_hi,steps", [
-    ("pbb", 1, 128, 32, 8, 2048, 0, 2048, 300000, 6),   # c3's heads, one sequence: 4 splits
+    ("pbb", 1, 128, 32, 8, 2048, 0, 2048, 300000, 6),   # c3's heads, one sequence: 8 splits
     ("pbb", 1, 128, 32, 8, 2048, 0, 2048, 0, 40),       # from position 0: mostly empty splits
-    ("pbb", 3, 64, 12, 2, 1024, 0, 1024, 5000, 8),      # 2 splits
+    ("pbb", 3, 64, 12, 2, 1024, 0, 1024, 5000, 8),      # 4 splits
     ("swa", 2, 128, 8, 2, 0, 4096, 4096, 300000, 4),    # 8 splits
+    ("pbb", 8, 128, 32, 8, 2048, 0, 2048, 300000, 3),   # 64 units: 4 splits
+    ("swa", 10, 64, 16, 4, 0, 1000, 1024, 90000, 3),    # 40 units: 4 splits
 ])
 def test_split_workgroups_small_batch(cuda, mode, batch, d, hq, hkv, block, window, slots,
                                       pos_hi, steps):

@@ -124,7 +124,7 @@ def test_rope_graph_replay_matches_eager(cuda):
 
 
 def test_rope_split_launch(cuda):
-    """Rotary decode in a split launch (one sequence at c3's head shapes: each unit over four
+    """Rotary decode in a split launch (one sequence at c3's head shapes: each unit over eight
     workgroups): the workgroup that owns the current token's step patches the turned key, the
     first workgroup appends it."""
     cfg = _cfg("pbb", 1, 32, 8, 128, 2048, pos_hi=1 << 20, steps=5, prefill=True)
