@@ -91,15 +91,18 @@ class Workload:
             self.desc = P.make_desc(cfg.batch, cfg.hq, cfg.hkv, cfg.d, window=cfg.window,
                                     slots=cfg.slots, dtype=dt, rope_base=cfg.rope_base)
             self.fn = P.swa_decode_step
+            self.fn_advance = P.swa_decode_step_advance
         else:
             self.desc = P.make_desc(cfg.batch, cfg.hq, cfg.hkv, cfg.d, block=cfg.block, dtype=dt,
                                     rope_base=cfg.rope_base)
             self.fn = P.pbb_decode_step
+            self.fn_advance = P.pbb_decode_step_advance
         self.k_ring, self.v_ring = P.alloc_rings(self.desc, device)
         self.ws = P.alloc_workspace(self.desc, device)
         P.ring_init(self.desc, self.k_ring, self.v_ring)
         self.pos0 = t0.to(torch.int32).to(device)
         self.pos = self.pos0.clone()
+        self.pos_next = torch.empty_like(self.pos)
         L = self.desc.slots
         ks = W.kv_window(cfg, "k", t0, L, device=device)
         vs = W.kv_window(cfg, "v", t0, L, device=device)
@@ -118,7 +121,11 @@ class Workload:
         self.fn(self.desc, self.pos, q, k, v, self.k_ring, self.v_ring, self.out, self.ws)
 
     def timed(self, warmup, steps):
-        """Returns (elapsed seconds of the whole loop, mean kernel seconds, algorithmic bytes)."""
+        """Returns (elapsed seconds of the whole loop, mean kernel seconds, algorithmic bytes).
+
+        A timed step is one launch: the positions advance on the device inside the decode
+        kernel (``*_decode_step_advance`` writing pos + 1 into a second position buffer, the two
+        buffers alternating), as the paper's decode loop advances them on the device."""
         import torch
         for i in range(warmup):
             self.step(i)
@@ -131,14 +138,19 @@ class Workload:
         for i in range(steps):
             total_bytes += step_bytes(t_first + i, self.cfg)
         torch.cuda.synchronize()
+        bufs = (self.pos, self.pos_next)
         w0 = time.perf_counter()
         for i in range(steps):
+            j = warmup + i
             starts[i].record()
-            self.step(warmup + i)
+            self.fn_advance(self.desc, bufs[i % 2], bufs[(i + 1) % 2], self.inputs[0][j],
+                            self.inputs[1][j], self.inputs[2][j], self.k_ring, self.v_ring,
+                            self.out, self.ws)
             ends[i].record()
-            self.pos += 1
         torch.cuda.synchronize()
         elapsed = time.perf_counter() - w0
+        if steps % 2:
+            self.pos.copy_(self.pos_next)   # self.pos holds the next position, as after step()
         kern = sum(s.elapsed_time(e) for s, e in zip(starts, ends)) / 1e3 / steps
         return elapsed, kern, total_bytes
 
