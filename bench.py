@@ -526,6 +526,8 @@ def main(argv=None):
                     help="only run the prefill measurements (c3 head shapes and paper shape)")
     ap.add_argument("--backward", action="store_true",
                     help="only run the training-backward measurements (same shapes as prefill)")
+    ap.add_argument("--batch-sweep", action="store_true",
+                    help="only run the decode at c3's head shapes for batches 16..1024")
     ap.add_argument("--small-batch", action="store_true",
                     help="only run the small-batch latency graphs (batches 1, 4, 8, 16 at c3's "
                          "head shapes; split launches up to 64 units)")
@@ -578,6 +580,22 @@ def main(argv=None):
     if args.paper_latency:
         print(json.dumps({"paper_shape_latency_us_per_step":
                           paper_latency(device, origins=PAPER_ORIGINS)}), flush=True)
+        return 0
+
+    if args.batch_sweep:
+        res = {}
+        for batch in (16, 32, 64, 128, 256, 512, 1024):
+            c = W.get_config("c3").with_(batch=batch)
+            wl = Workload(c, W.initial_positions(c), 60, device)
+            el, ks, tb = wl.timed(10, 50)
+            res[f"batch{batch}"] = {"kernel_us": ks * 1e6, "tokens_per_s": batch * 50 / el,
+                                    "hbm_gbps_kernel": tb / 50 / ks / 1e9,
+                                    "frac_of_peak": tb / 50 / ks / 1e9 / HBM_PEAK_GBPS,
+                                    "workspace_bytes": 0 if wl.ws is None else wl.ws.numel()}
+            print(f"[bench] batch {batch}: {ks * 1e6:.1f} us", file=sys.stderr, flush=True)
+            del wl
+            torch.cuda.empty_cache()
+        print(json.dumps({"batch_sweep_c3_heads": res}), flush=True)
         return 0
 
     if args.small_batch:
