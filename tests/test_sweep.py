@@ -46,10 +46,20 @@ def _decode_cases(n=24, seed=2024):
 
 @pytest.mark.parametrize("i,mode,d,G,hkv,batch,block,window,slots,far", _decode_cases())
 def test_decode_sweep(cuda, i, mode, d, G, hkv, batch, block, window, slots, far):
+    _decode_sweep_case(cuda, "bf16", i, mode, d, G, hkv, batch, block, window, slots, far)
+
+
+@pytest.mark.parametrize("i,mode,d,G,hkv,batch,block,window,slots,far",
+                         _decode_cases(12, seed=77))
+def test_decode_sweep_f32(cuda, i, mode, d, G, hkv, batch, block, window, slots, far):
+    _decode_sweep_case(cuda, "f32", i, mode, d, G, hkv, batch, block, window, slots, far)
+
+
+def _decode_sweep_case(cuda, dtype, i, mode, d, G, hkv, batch, block, window, slots, far):
     steps = 3
-    cfg = W.Config(f"sweep{i}-{mode}-{d}-{G}x{hkv}-b{batch}-{block}-{window}-{slots}", mode,
-                   batch=batch, hq=G * hkv, hkv=hkv, d=d, block=block, slots=slots,
-                   window=window, dtype="bf16", seed=100 + i, value_scale=1.0,
+    cfg = W.Config(f"sweep{i}-{dtype}-{mode}-{d}-{G}x{hkv}-b{batch}-{block}-{window}-{slots}",
+                   mode, batch=batch, hq=G * hkv, hkv=hkv, d=d, block=block, slots=slots,
+                   window=window, dtype=dtype, seed=100 + i, value_scale=1.0,
                    pos_hi=(1 << 20) if far else 3 * (block or window) + 5, steps=steps,
                    prefill=True)
     t0 = W.initial_positions(cfg)
