@@ -55,11 +55,20 @@ def test_decode_sweep_f32(cuda, i, mode, d, G, hkv, batch, block, window, slots,
     _decode_sweep_case(cuda, "f32", i, mode, d, G, hkv, batch, block, window, slots, far)
 
 
-def _decode_sweep_case(cuda, dtype, i, mode, d, G, hkv, batch, block, window, slots, far):
+@pytest.mark.parametrize("i,mode,d,G,hkv,batch,block,window,slots,far",
+                         _decode_cases(8, seed=99))
+def test_decode_sweep_rope(cuda, i, mode, d, G, hkv, batch, block, window, slots, far):
+    _decode_sweep_case(cuda, "bf16", i, mode, d, G, hkv, batch, block, window, slots, far,
+                       rope=(1e4, 1e6)[i % 2])
+
+
+def _decode_sweep_case(cuda, dtype, i, mode, d, G, hkv, batch, block, window, slots, far,
+                       rope=0.0):
     steps = 3
-    cfg = W.Config(f"sweep{i}-{dtype}-{mode}-{d}-{G}x{hkv}-b{batch}-{block}-{window}-{slots}",
-                   mode, batch=batch, hq=G * hkv, hkv=hkv, d=d, block=block, slots=slots,
-                   window=window, dtype=dtype, seed=100 + i, value_scale=1.0,
+    cfg = W.Config(f"sweep{i}-{dtype}-{mode}-{d}-{G}x{hkv}-b{batch}-{block}-{window}-{slots}"
+                   f"-rope{rope:g}", mode, batch=batch, hq=G * hkv, hkv=hkv, d=d, block=block,
+                   slots=slots, window=window, dtype=dtype, seed=100 + i, value_scale=1.0,
+                   rope_base=rope,
                    pos_hi=(1 << 20) if far else 3 * (block or window) + 5, steps=steps,
                    prefill=True)
     t0 = W.initial_positions(cfg)
@@ -70,9 +79,15 @@ def _decode_sweep_case(cuda, dtype, i, mode, d, G, hkv, batch, block, window, sl
     for s in range(steps):
         q, out = run.step()
         compare(cfg, to_np(out), run.oracle_out(rows, s, q, hist=hist), what=f"{cfg.name} step {s}")
-    for which in ("k", "v"):
+    for which in (("v",) if rope else ("k", "v")):
         exp = run.expected_ring(rows, steps - 1, which, hist=hist)
         assert np.array_equal(run.ring_rows(rows, which), exp), f"{cfg.name} ring {which}"
+    if rope:
+        # rotated keys: within one bf16 rounding of their exact rotation
+        exact = run.expected_rotated_keys(rows, steps - 1, hist=hist)
+        got = run.ring_rows(rows, "k").view(np.uint16).astype(np.uint32) << 16
+        err = np.abs(got.view(np.float32).astype(np.float64) - exact)
+        assert (err <= np.abs(exact) * 2.0 ** -8 + 1e-6).all(), f"{cfg.name} rotated keys"
 
 
 def _prompt_cases(n=12, seed=7):
