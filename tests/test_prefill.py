@@ -104,26 +104,34 @@ def test_prefill_without_optional_outputs(cuda):
     compare(cfg, to_np(out), ref, what="no lse, no rings")
 
 
-def test_prefill_then_decode_continues(cuda):
+@pytest.mark.parametrize("mode,batch,hq,hkv,d,block,window,slots,n,steps", [
+    ("pbb", 2, 8, 2, 128, 128, 0, 128, 700, 70),
+    ("swa", 2, 8, 2, 64, 0, 100, 128, 700, 70),          # ring larger than the window
+    ("pbb", 1, 32, 8, 128, 2048, 0, 2048, 3000, 20),     # decode as a split launch
+])
+def test_prefill_then_decode_continues(cuda, mode, batch, hq, hkv, d, block, window, slots, n,
+                                       steps):
     """Rings written by prefill are the state decode needs: steps at positions n, n+1, ...
     match the oracle over prompt plus appended tokens."""
-    n, steps = 700, 70
-    cfg = _cfg("pbb", 2, n + steps, 8, 2, 128, 128)
+    cfg = _cfg(mode, batch, n + steps, hq, hkv, d, block, window, slots)
     desc, (q, k, v), out, lse, kr, vr = _run(cfg, n, cuda)
     qa, ka, va = W.prompt(cfg, n + steps, device=cuda)   # positions 0 .. n+steps-1
     pos = torch.full((cfg.batch,), n, dtype=torch.int32, device=cuda)
     kh = ka.permute(0, 2, 1, 3).contiguous()
     vh = va.permute(0, 2, 1, 3).contiguous()
+    step = P.swa_decode_step if mode == "swa" else P.pbb_decode_step
+    m = oracle.SWA if mode == "swa" else oracle.PBB
     for i in range(steps):
         t = n + i
         qd = qa[:, t].contiguous()
         o = torch.empty_like(qd)
-        P.pbb_decode_step(desc, pos, qd, ka[:, t].contiguous(), va[:, t].contiguous(), kr, vr, o)
+        step(desc, pos, qd, ka[:, t].contiguous(), va[:, t].contiguous(), kr, vr, o)
         pos += 1
         if i % 7 == 0 or i == steps - 1:
-            ref = oracle.decode(oracle.PBB, np.full(cfg.batch, t), to_np(qd), to_np(kh[:, :, :t + 1]),
-                                to_np(vh[:, :, :t + 1]), np.zeros(cfg.batch, np.int64), block=128)
-            compare(cfg, to_np(o), ref, what=f"decode after prefill, t={t}")
+            ref = oracle.decode(m, np.full(cfg.batch, t), to_np(qd), to_np(kh[:, :, :t + 1]),
+                                to_np(vh[:, :, :t + 1]), np.zeros(cfg.batch, np.int64),
+                                block=block, window=window)
+            compare(cfg, to_np(o), ref, what=f"{mode} decode after prefill, t={t}")
 
 
 def test_prefill_is_deterministic_and_leaves_inputs(cuda):
