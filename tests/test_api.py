@@ -272,3 +272,35 @@ def test_split_decode_workspace():
     assert lib.pbb_decode_step(*args, vp(0), ctypes.c_size_t(0), vp(0)) == 5
     assert lib.pbb_decode_step(*args, vp(A), ctypes.c_size_t(P.workspace_bytes(one) - 1), vp(0)) == 5
     assert lib.pbb_decode_step(*args, vp(A + 8), ctypes.c_size_t(1 << 24), vp(0)) == 4
+
+
+def test_split_rule_over_random_descriptors():
+    """The documented split rule, restated: bf16 launches with at most 64 (sequence, KV head)
+    units split each unit over S = min(ceil(256 / units), ceil(steps / 8), 8) workgroups
+    (steps = ceil(B / 32) or ceil(W / 32)); S > 1 needs 256-byte-aligned counters plus
+    units * S * G * (d + 2) floats."""
+    import numpy as np
+    rng = np.random.default_rng(3)
+    for _ in range(400):
+        batch = int(rng.integers(1, 80))
+        hkv = int(rng.choice([1, 2, 4, 8]))
+        G = int(rng.integers(1, 17))
+        d = int(rng.choice([64, 128]))
+        swa = bool(rng.integers(0, 2))
+        span = int(rng.choice([2, 64, 256, 258, 300, 1024, 2048, 4096, 65536]))
+        dt = torch.bfloat16 if rng.integers(0, 4) else torch.float32
+        if swa:
+            desc = B.make_desc(batch, G * hkv, hkv, d, window=span, slots=span, dtype=dt)
+            got = P.swa_workspace_bytes(desc)
+        else:
+            desc = B.make_desc(batch, G * hkv, hkv, d, block=span, dtype=dt)
+            got = P.workspace_bytes(desc)
+        units = batch * hkv
+        steps = -(-span // 32)
+        S = min(-(-256 // units), -(-steps // 8), 8) if units <= 64 else 1
+        if dt != torch.bfloat16 or S <= 1:
+            assert got == 0, (batch, hkv, G, d, swa, span, dt)
+            continue
+        counters = -(-(units * 4) // 256) * 256
+        part = units * S * G * (d + 2) * 4
+        assert got == counters + -(-part // 256) * 256, (batch, hkv, G, d, swa, span)
