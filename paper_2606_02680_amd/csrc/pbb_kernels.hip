@@ -254,6 +254,187 @@ __global__ __launch_bounds__(256) void decode_f32_kernel(DecodeArgs a) {
 }
 
 // ------------------------------------------------------------------------------------------
+// fp32 decode on matrix cores (v_mfma_f32_16x16x4_f32: fp32 operands and accumulation).
+//
+// One workgroup of NW waves per (sequence, KV head); wave w handles 16-key tiles w, w + NW, ...
+// of the unit's key list (ring keys, then the current token).  Rows travel from memory straight
+// into registers as matrix-core operands, the next tile's loads in flight while the current tile
+// computes.  Lane l works in quarter j = l / 16 on row l % 16 of each 16 x 16 tile:
+//   scores  S^T[16 keys][16 heads] = K Q^T in D/4 MFMAs; MFMA m contracts channel
+//           (D/4) j + m in quarter j, so lane (key l%16, j) reads D/4 consecutive channels of
+//           its key row, and the B operand holds the queries (scaled by scale * log2 e, zero for
+//           heads past G).  The result gives lane (head l%16, j) keys 4j..4j+3 of the tile.
+//   softmax column maxima across the quarters by permlane swaps; the reference moves only when
+//           a column's maximum exceeds it by more than 8 (log2 units), decided wave-uniformly.
+//   values  O^T += V^T P^T in D/4 MFMAs: row r of output tile nb is channel (D/16) r + nb and
+//           MFMA (nb, m) contracts key 4j + m in quarter j, so the B operand is the lane's own
+//           weight of key 4j + m and lane (r, j) reads D/16 consecutive channels of each of
+//           its four key rows.
+// Waves merge through LDS with Eq.(lse) (Appendix A.4); the append of the current token is
+// done last (its slot is never read in the launch).
+// Groups from this size on take the matrix-core fp32 kernel (a single query head per KV head
+// streams as fast on the vector ALUs).
+constexpr int kF32MatrixMinGroup = 2;
+
+template <int D, int NW>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2)))
+void decode_f32_mfma_kernel(DecodeArgs a) {
+  constexpr int KM = D / 4;     // MFMAs per score tile (channels per quarter)
+  constexpr int E = D / 16;     // output tiles; channels per lane per key row of V
+  constexpr int KQ = KM / 4;    // float4 loads of a lane's K channels
+  constexpr int VQ = E / 4;     // float4 loads per V row
+  typedef float f4 __attribute__((ext_vector_type(4)));
+  __shared__ float sm_acc[NW][16][D];
+  __shared__ float sm_m[NW][16];
+  __shared__ float sm_l[NW][16];
+
+  const int bg = blockIdx.x;
+  const int b = bg / a.hkv;
+  const int g = bg - b * a.hkv;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int c16 = lane & 15;
+  const int j4 = lane >> 4;
+  const int G = a.group;
+  float* out = (float*)a.out + ((size_t)b * a.hq + (size_t)g * G) * D;
+  const int t = a.pos[b];
+  if (t < 0) {
+    for (int e = tid; e < G * D; e += NW * 64) out[e] = 0.0f;
+    if (a.pos_next != nullptr && g == 0 && tid == 0) a.pos_next[b] = t;
+    return;
+  }
+  const Ranges R = ranges_for(a, t);
+  if (a.pos_next != nullptr && g == 0 && tid == 0) a.pos_next[b] = t + 1;
+  float* kring = (float*)a.k_ring + (size_t)bg * a.slots * D;
+  float* vring = (float*)a.v_ring + (size_t)bg * a.slots * D;
+  const float* knew = (const float*)a.k_new + (size_t)bg * D;
+  const float* vnew = (const float*)a.v_new + (size_t)bg * D;
+  const int n_total = R.n_ring + 1;
+  const int ntiles = (n_total + 15) >> 4;
+
+  // Queries of head c16 (zero past G), channels (D/4) j4 + m, scaled into log2 units.
+  float qf[KM];
+  {
+    const float* qrow = (const float*)a.q + ((size_t)b * a.hq + (size_t)g * G +
+                                             (size_t)(c16 < G ? c16 : 0)) * D + KM * j4;
+#pragma unroll
+    for (int m = 0; m < KM; ++m) qf[m] = c16 < G ? qrow[m] * a.scale_log2 : 0.0f;
+  }
+  // Row of key i of the unit: a ring slot, the current token, or (past the end) the current
+  // token again, masked out of the softmax.
+  auto krow = [&](int i) __attribute__((always_inline)) -> const float* {
+    return i < R.n_ring ? kring + (size_t)ring_slot(R, i) * D : knew;
+  };
+  auto vrow = [&](int i) __attribute__((always_inline)) -> const float* {
+    return i < R.n_ring ? vring + (size_t)ring_slot(R, i) * D : vnew;
+  };
+  auto load = [&](int tile, f4 (&kb)[KQ], f4 (&vb)[4][VQ]) __attribute__((always_inline)) {
+    const int i0 = tile * 16;
+    const float* kp = krow(i0 + c16) + KM * j4;
+#pragma unroll
+    for (int q = 0; q < KQ; ++q) kb[q] = *(const f4*)(kp + 4 * q);
+#pragma unroll
+    for (int m = 0; m < 4; ++m) {
+      const float* vp = vrow(i0 + 4 * j4 + m) + E * c16;
+#pragma unroll
+      for (int q = 0; q < VQ; ++q) vb[m][q] = *(const f4*)(vp + 4 * q);
+    }
+  };
+
+  float mref = -1.0e30f;   // finite floor below any score: masked keys weigh exp2(-inf) = 0
+  float lsum = 0.0f;
+  f4 acc[E];
+#pragma unroll
+  for (int nb = 0; nb < E; ++nb) acc[nb] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+
+  auto compute = [&](int tile, const f4 (&kb)[KQ], const f4 (&vb)[4][VQ])
+      __attribute__((always_inline)) {
+    f4 s = f4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int m = 0; m < KM; ++m)
+      s = __builtin_amdgcn_mfma_f32_16x16x4f32(kb[m >> 2][m & 3], qf[m], s, 0, 0, 0);
+    const int i0 = tile * 16 + 4 * j4;
+    float mx = kNegInf;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      s[e] = i0 + e < n_total ? s[e] : kNegInf;
+      mx = fmaxf(mx, s[e]);
+    }
+    mx = max_xor16_32(mx);
+    const bool grow = mx > mref + 8.0f;
+    if (__builtin_amdgcn_ballot_w64(grow) != 0) {
+      const float alpha = grow ? fast_exp2(mref - mx) : 1.0f;
+      mref = grow ? mx : mref;
+      lsum *= alpha;
+#pragma unroll
+      for (int nb = 0; nb < E; ++nb) acc[nb] *= alpha;
+    }
+    float p[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      p[e] = fast_exp2(s[e] - mref);
+      lsum += p[e];
+    }
+#pragma unroll
+    for (int nb = 0; nb < E; ++nb)
+#pragma unroll
+      for (int m = 0; m < 4; ++m)
+        acc[nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(vb[m][nb >> 2][nb & 3], p[m], acc[nb],
+                                                      0, 0, 0);
+  };
+
+  f4 ka[KQ], kb2[KQ];
+  f4 va[4][VQ], vb2[4][VQ];
+  int tile = wave;
+  if (tile < ntiles) load(tile, ka, va);
+  while (tile < ntiles) {
+    if (tile + NW < ntiles) load(tile + NW, kb2, vb2);
+    compute(tile, ka, va);
+    tile += NW;
+    if (tile >= ntiles) break;
+    if (tile + NW < ntiles) load(tile + NW, ka, va);
+    compute(tile, kb2, vb2);
+    tile += NW;
+  }
+
+  // Column sum over the four quarters; then the waves merge through LDS.
+  lsum = sum_xor16_32(lsum);
+  if (c16 < G) {
+#pragma unroll
+    for (int nb = 0; nb < E; ++nb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) sm_acc[wave][c16][E * (4 * j4 + i) + nb] = acc[nb][i];
+    if (j4 == 0) {
+      sm_m[wave][c16] = mref;
+      sm_l[wave][c16] = lsum;
+    }
+  }
+  __syncthreads();
+  for (int idx = tid; idx < G * D; idx += NW * 64) {
+    const int h = idx / D;
+    const int c = idx - h * D;
+    float M = kNegInf;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) M = fmaxf(M, sm_m[w][h]);
+    float L = 0.0f, O = 0.0f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      const float wt = fast_exp2(sm_m[w][h] - M);   // idle waves hold the floor: weight 0
+      L += wt * sm_l[w][h];
+      O += wt * sm_acc[w][h][c];
+    }
+    out[idx] = O / L;
+  }
+
+  // Fused append of the current token (slot t mod slots is outside the support).
+  if (wave == 0 && lane < D / 4) {
+    *(f4*)(kring + (size_t)R.append_slot * D + 4 * lane) = *(const f4*)(knew + 4 * lane);
+    *(f4*)(vring + (size_t)R.append_slot * D + 4 * lane) = *(const f4*)(vnew + 4 * lane);
+  }
+}
+
+// ------------------------------------------------------------------------------------------
 // bf16 decode on matrix cores.
 //
 // One workgroup of NW waves per (sequence, KV head); wave w handles 32-key steps
@@ -828,6 +1009,13 @@ hipError_t launch_decode_bf16(const DecodeArgs& a, int32_t head_dim, hipStream_t
 
 hipError_t launch_decode_f32(const DecodeArgs& a, int32_t head_dim, hipStream_t stream) {
   const dim3 grid((unsigned)(a.batch * a.hkv));
+  if (a.group >= kF32MatrixMinGroup) {
+    if (head_dim == 128)
+      hipLaunchKernelGGL((decode_f32_mfma_kernel<128, 4>), grid, dim3(256), 0, stream, a);
+    else
+      hipLaunchKernelGGL((decode_f32_mfma_kernel<64, 4>), grid, dim3(256), 0, stream, a);
+    return hipGetLastError();
+  }
   const dim3 block(256);
   if (head_dim == 128) {
     if (a.group <= 4)
