@@ -350,10 +350,16 @@ void decode_f32_mfma_kernel(DecodeArgs a) {
 
   auto compute = [&](int tile, const f4 (&kb)[KQ], const f4 (&vb)[4][VQ])
       __attribute__((always_inline)) {
-    f4 s = f4{0.0f, 0.0f, 0.0f, 0.0f};
+    // Four partial dot products (channels m mod 4), summed pairwise: chains of D/16
+    // accumulations instead of D/4 keep the fp32 rounding of the scores at the level of a
+    // short sum (one chain of D/4 doubled the largest output error at c4's shapes).
+    f4 sp[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) sp[u] = f4{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
     for (int m = 0; m < KM; ++m)
-      s = __builtin_amdgcn_mfma_f32_16x16x4f32(kb[m >> 2][m & 3], qf[m], s, 0, 0, 0);
+      sp[m & 3] = __builtin_amdgcn_mfma_f32_16x16x4f32(kb[m >> 2][m & 3], qf[m], sp[m & 3], 0, 0, 0);
+    f4 s = (sp[0] + sp[1]) + (sp[2] + sp[3]);
     const int i0 = tile * 16 + 4 * j4;
     float mx = kNegInf;
 #pragma unroll

@@ -122,6 +122,14 @@ def test_c4_ragged_spiked_sampled(cuda):
     print(f"c4 {worst}")
 
 
+def test_c4_shapes_fp32_sampled(cuda):
+    """c4's shapes and tensors with fp32 rings and I/O (the matrix-core fp32 kernel at its
+    full launch size, G = 8): sampled sequences at forced edge positions, 1e-5."""
+    cfg = W.get_config("c4").with_(dtype="f32", name="c4-shapes-fp32")
+    _, _, _, worst = _sampled(cfg, cuda, steps=2, n_rows=24)
+    print(f"c4 fp32 {worst}")
+
+
 def test_c5_swa_sampled(cuda):
     cfg = W.get_config("c5")
     _, _, _, worst = _sampled(cfg, cuda, steps=2, n_rows=16)
