@@ -526,6 +526,8 @@ def main(argv=None):
                     help="only run the prefill measurements (c3 head shapes and paper shape)")
     ap.add_argument("--backward", action="store_true",
                     help="only run the training-backward measurements (same shapes as prefill)")
+    ap.add_argument("--fp32", action="store_true",
+                    help="only run fp32 decode at c3's and c4's shapes (and G = 1 variants)")
     ap.add_argument("--batch-sweep", action="store_true",
                     help="only run the decode at c3's head shapes for batches 16..1024")
     ap.add_argument("--small-batch", action="store_true",
@@ -580,6 +582,22 @@ def main(argv=None):
     if args.paper_latency:
         print(json.dumps({"paper_shape_latency_us_per_step":
                           paper_latency(device, origins=PAPER_ORIGINS)}), flush=True)
+        return 0
+
+    if args.fp32:
+        res = {}
+        for name, over in (("c3", {}), ("c4", {}), ("c3", {"hq": 8}), ("c4", {"hq": 2, "batch": 512})):
+            c = W.get_config(name).with_(dtype="f32", **over)
+            wl = Workload(c, W.initial_positions(c), 60, device)
+            el, ks, tb = wl.timed(10, 50)
+            key = f"{name}_shapes_fp32_G{c.hq // c.hkv}_batch{c.batch}"
+            res[key] = {"kernel_us": ks * 1e6, "tokens_per_s": c.batch * 50 / el,
+                        "hbm_gbps_kernel": tb / 50 / ks / 1e9,
+                        "frac_of_peak": tb / 50 / ks / 1e9 / HBM_PEAK_GBPS}
+            print(f"[bench] {key}: {ks * 1e6:.1f} us", file=sys.stderr, flush=True)
+            del wl
+            torch.cuda.empty_cache()
+        print(json.dumps({"fp32_decode": res}), flush=True)
         return 0
 
     if args.batch_sweep:
