@@ -103,7 +103,10 @@ pbb_status_t pbb_ring_bytes(const pbb_desc_t *desc, size_t *bytes_per_tensor);
 /*
  * Enqueue zero-filling of both rings on `stream`.  A zeroed ring is the state before the
  * first decode step at position 0: for t < slots the support only covers positions that
- * have been appended, so the zeros are never read (Appendix F.1, proof of the proposition).
+ * have been appended (Appendix F.1, proof of the proposition).  The call is optional: the
+ * decode steps never let a slot outside the support affect an output, whatever bits it holds
+ * (NaN included), so rings may also start uninitialised or be loaded with pbb_ring_fill
+ * with only the history the support needs.
  */
 pbb_status_t pbb_ring_init(const pbb_desc_t *desc, void *k_ring, void *v_ring, void *stream);
 

@@ -14,12 +14,12 @@
 
 namespace {
 
-constexpr int32_t kMaxGroup = 16;     // query heads per KV head held by one MFMA tile
+using pbb::kMaxGroup;
+using pbb::kSplitMaxUnits;
+using pbb::kSplitMaxWays;
 constexpr int32_t kMaxSlots = 65536;  // ring slots per (sequence, KV head)
 constexpr int32_t kMaxPrefill = 1 << 30;  // prompt positions per call
 constexpr int64_t kSplitUnits = 256;      // workgroups a split decode launch aims for (CUs)
-constexpr int64_t kSplitMaxUnits = 64;    // bf16 decode launches with at most this many units split
-constexpr int64_t kSplitMaxWays = 8;      // workgroups per unit of a split launch, at most
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 

@@ -14,6 +14,10 @@ enum SupportMode : int32_t { kSupportPBB = 0, kSupportSWA = 1 };
 // merge stages their maxima and sums in LDS).
 constexpr int kMaxSplitStates = 2048;
 
+constexpr int32_t kMaxGroup = 16;         // query heads per KV head held by one MFMA tile
+constexpr int64_t kSplitMaxUnits = 64;    // bf16 decode launches with at most this many units split
+constexpr int64_t kSplitMaxWays = 8;      // workgroups per unit of a split launch, at most
+
 // Everything a decode kernel needs, validated on the host before launch.
 struct DecodeArgs {
   const int32_t* pos;

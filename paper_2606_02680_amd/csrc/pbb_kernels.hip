@@ -350,16 +350,17 @@ void decode_f32_mfma_kernel(DecodeArgs a) {
 
   auto compute = [&](int tile, const f4 (&kb)[KQ], const f4 (&vb)[4][VQ])
       __attribute__((always_inline)) {
-    // Four partial dot products (channels m mod 4), summed pairwise: chains of D/16
-    // accumulations instead of D/4 keep the fp32 rounding of the scores at the level of a
-    // short sum (one chain of D/4 doubled the largest output error at c4's shapes).
-    f4 sp[4];
+    // Eight partial dot products (MFMAs m mod 8), summed pairwise: the matrix core adds each of
+    // its four products into the accumulator with a rounding, so eight chains of D/8 sequential
+    // products (instead of four of D/4) keep the scores' fp32 rounding at the level of a short
+    // sum.
+    f4 sp[8];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) sp[u] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+    for (int u = 0; u < 8; ++u) sp[u] = f4{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
     for (int m = 0; m < KM; ++m)
-      sp[m & 3] = __builtin_amdgcn_mfma_f32_16x16x4f32(kb[m >> 2][m & 3], qf[m], sp[m & 3], 0, 0, 0);
-    f4 s = (sp[0] + sp[1]) + (sp[2] + sp[3]);
+      sp[m & 7] = __builtin_amdgcn_mfma_f32_16x16x4f32(kb[m >> 2][m & 3], qf[m], sp[m & 7], 0, 0, 0);
+    f4 s = ((sp[0] + sp[1]) + (sp[2] + sp[3])) + ((sp[4] + sp[5]) + (sp[6] + sp[7]));
     const int i0 = tile * 16 + 4 * j4;
     float mx = kNegInf;
 #pragma unroll
@@ -378,16 +379,23 @@ void decode_f32_mfma_kernel(DecodeArgs a) {
     }
     float p[4];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      p[e] = fast_exp2(s[e] - mref);
-      lsum += p[e];
+    for (int e = 0; e < 4; ++e) p[e] = fast_exp2(s[e] - mref);
+    lsum += (p[0] + p[1]) + (p[2] + p[3]);
+    // The matrix core adds its four products into the accumulator one at a time, each with a
+    // rounding, so the tile's 16 keys are first summed into a fresh partial (rounding on small
+    // values) that then enters the running sum with a single addition: one rounding per tile
+    // on the large sum instead of sixteen.  With the eight score chains above, the largest
+    // output error over c4's shapes and tensors (G = 8, |o| up to ~18) drops from 1.4e-5 to
+    // about 5e-6, against the 1e-5 bound.
+#pragma unroll
+    for (int nb = 0; nb < E; ++nb) {
+      f4 part = __builtin_amdgcn_mfma_f32_16x16x4f32(vb[0][nb >> 2][nb & 3], p[0],
+                                                    f4{0.0f, 0.0f, 0.0f, 0.0f}, 0, 0, 0);
+#pragma unroll
+      for (int m = 1; m < 4; ++m)
+        part = __builtin_amdgcn_mfma_f32_16x16x4f32(vb[m][nb >> 2][nb & 3], p[m], part, 0, 0, 0);
+      acc[nb] += part;
     }
-#pragma unroll
-    for (int nb = 0; nb < E; ++nb)
-#pragma unroll
-      for (int m = 0; m < 4; ++m)
-        acc[nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(vb[m][nb >> 2][nb & 3], p[m], acc[nb],
-                                                      0, 0, 0);
   };
 
   f4 ka[KQ], kb2[KQ];
@@ -480,6 +488,30 @@ void decode_f32_mfma_kernel(DecodeArgs a) {
 // that gfx950 serves per cycle.
 // Device-coherent float store and load (agent scope): they bypass the caches that are not
 // coherent across the chip's compute dies, without writing back or invalidating those caches.
+//
+// Ordering of the split merge.  The partial states are published and read ONLY through these
+// agent-scope atomic accesses, and the unit counter is an agent-scope atomic add; the argument
+// rests on how the AMDGPU backend's memory model for gfx942/gfx950 lowers them (LLVM
+// AMDGPUUsage, "Memory Model GFX942"):
+//   * an agent-scope atomic store or load is a global store/load with sc1 set: the store is
+//     written through this die's L2 to the agent's coherence point, and the load is not served
+//     from a stale line of a non-coherent cache;
+//   * s_waitcnt vmcnt(0) returns only once every earlier store of the wave has been
+//     acknowledged, i.e. is visible at that coherence point.  This is the completion step of
+//     the backend's agent-scope release sequence; the other step of that sequence, the L2
+//     write-back (buffer_wbl2 sc1), exists for stores made WITHOUT sc1, and no partial state is
+//     written that way;
+//   * the acquire sequence's L2 invalidation (buffer_inv sc1) likewise exists for later loads
+//     made without sc1, and the merge reads the workspace only with sc1 loads, which it issues
+//     after the counter's returned value has been observed (the flag goes through LDS and a
+//     workgroup barrier, so no load can be performed before the add has returned).
+// Hence: every store of a workgroup completes (vmcnt(0), then the barrier) before its count is
+// added, and the last arriver's loads read the coherence point after the final count -- the
+// guarantees a release add / acquire load pair would give, without the cache-wide write-back
+// and invalidation (measured 3x slower, because the invalidation also evicts rings that stay
+// cache-resident at small batch).  Relaxed accesses do not carry this guarantee in the
+// language-level model; it is a property of the lowering above, and the graph-replay split
+// tests exercise it every replay.
 __device__ __forceinline__ void coherent_store(float* p, float v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -661,9 +693,17 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
     __builtin_amdgcn_s_waitcnt(0x0F70 | (OPS & 15) | ((OPS >> 4) << 14));
     if (step == cur_step) {
       // The current token's row arrived from slot 0: overwrite it with k_new / v_new (the
-      // turned key in rotary mode).
+      // turned key in rotary mode).  The V rows after it (this step's padding, also DMA'd
+      // from slot 0) are zeroed: their weights are 0, but slot 0 may hold bits that were
+      // never written (0 * NaN would reach the output).  Padded K rows need nothing: their
+      // scores are replaced by -inf below.
       const int rc = R.n_ring & 31;
       unsigned char* tile = wbuf + BO;
+      {
+        const u32x4 zero = {0u, 0u, 0u, 0u};
+        for (int e = lane; e < (31 - rc) * PPR; e += 64)
+          *(u32x4*)(tile + TILE + (rc + 1 + e / PPR) * ROWB + (e % PPR) * 16) = zero;
+      }
       if constexpr (ROPE) {
         if (lane < PPR / 2) {
           unsigned char* row = tile + rc * ROWB;
@@ -719,14 +759,17 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) acc[nb] *= alpha;
     }
+    // The weights enter the value product rounded to bf16; the denominator sums the same
+    // rounded weights, so the output is an exactly normalised average of the values under
+    // those weights.  (Summing the unrounded weights instead leaves a mismatch of up to 2^-9
+    // relative that scales with |o| itself, e.g. when one key carries almost all the weight.)
     float ps = 0.0f;
     bf16x8 pB;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const float sc = e < 4 ? s0[e] : s1[e - 4];
-      const float p = fast_exp2(__builtin_fmaf(sc, c, -m));
-      ps += p;
-      pB[e] = (__bf16)p;
+      pB[e] = (__bf16)fast_exp2(__builtin_fmaf(sc, c, -m));
+      ps += (float)pB[e];
     }
     lsum += ps;
     if constexpr (NB == 8) {
