@@ -31,6 +31,64 @@ def bf16_tolerance_ok(got: np.ndarray, ref: np.ndarray):
     return np.abs(got - ref) <= 2e-2 + np.abs(ref) * 2.0 ** -8
 
 
+def bf16_round(x: np.ndarray) -> np.ndarray:
+    """Round float64 values to the nearest bfloat16 (8 significant bits), ties to even,
+    directly from float64 (no intermediate float32 rounding)."""
+    x = np.asarray(x, dtype=np.float64)
+    out = np.zeros_like(x)
+    nz = x != 0
+    e = np.floor(np.log2(np.abs(x[nz])))
+    ulp = np.exp2(e - 7)
+    out[nz] = np.round(x[nz] / ulp) * ulp   # np.round: half to even; the scaling is exact
+    return out
+
+
+def error_stats(got: np.ndarray, ref: np.ndarray) -> dict:
+    """Secondary error metrics of a comparison (the paper reports max abs, relative L2 and
+    cosine): strict max |got - ref|, max |got - bf16(ref)|, the largest |ref|, and the worst
+    relative L2 and cosine over (sequence, head) rows."""
+    got = got.astype(np.float64)
+    g = got.reshape(-1, got.shape[-1])
+    r = ref.reshape(-1, ref.shape[-1])
+    rn = np.linalg.norm(r, axis=1)
+    rel = np.linalg.norm(g - r, axis=1) / np.maximum(rn, 1e-30)
+    cos = (g * r).sum(1) / np.maximum(np.linalg.norm(g, axis=1) * rn, 1e-30)
+    err = np.abs(got - ref)
+    return {"max_abs": float(err.max()),
+            "argmax": [int(x) for x in np.unravel_index(np.argmax(err), err.shape)],
+            "max_abs_vs_bf16_ref": float(np.abs(got - bf16_round(ref)).max()),
+            "max_ref": float(np.abs(ref).max()),
+            "rel_l2_max": float(rel.max()), "cos_min": float(cos.min())}
+
+
+def merge_stats(a: dict | None, b: dict, where=None) -> dict:
+    """Worst-case merge of two error_stats results; ``argmax`` follows the larger max_abs and
+    is prefixed with ``where`` (e.g. step and first sequence of the chunk) when given."""
+    b = dict(b)
+    if where is not None and "argmax" in b:
+        b["argmax"] = list(where) + b["argmax"]
+    if a is None:
+        return b
+    out = {k: (min(a[k], b[k]) if k == "cos_min" else max(a[k], b[k]))
+           for k in b if k != "argmax"}
+    if "argmax" in b:
+        out["argmax"] = b["argmax"] if b["max_abs"] > a["max_abs"] else a["argmax"]
+    return out
+
+
+def record_stats(name: str, stats: dict):
+    """Print a parity record and append it to the JSON-lines file named by the environment
+    variable PBB_PARITY_RECORD, if set."""
+    import json
+    import os
+    line = json.dumps({"case": name, **stats})
+    print(f"[parity-stats] {line}", flush=True)
+    path = os.environ.get("PBB_PARITY_RECORD")
+    if path:
+        with open(path, "a") as f:
+            f.write(line + "\n")
+
+
 def compare(cfg: W.Config, got: np.ndarray, ref: np.ndarray, what: str = ""):
     """Assert the tolerance for the workload dtype; returns a metrics dict."""
     got = got.astype(np.float64)
