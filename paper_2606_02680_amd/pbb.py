@@ -8,7 +8,6 @@ status.  All computation happens in the library's HIP kernels; there is no fallb
 from __future__ import annotations
 
 import ctypes
-import math
 import os
 
 import torch
@@ -104,10 +103,27 @@ def make_desc(batch: int, n_q_heads: int, n_kv_heads: int, head_dim: int, *, blo
                    float(scale), float(rope_base))
 
 
-def _stream(stream):
+def _torch_stream(stream):
+    """The torch stream object of ``stream`` (None: torch's current stream; a raw hipStream_t
+    handle is wrapped as an external stream)."""
     if stream is None:
-        stream = torch.cuda.current_stream()
-    return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+        return torch.cuda.current_stream()
+    if hasattr(stream, "cuda_stream"):
+        return stream
+    return torch.cuda.ExternalStream(int(stream))
+
+
+def _stream(stream):
+    return ctypes.c_void_p(_torch_stream(stream).cuda_stream)
+
+
+def _scratch_on(stream, make):
+    """Allocate a temporary buffer with ``make()`` for a launch on ``stream``: the allocation
+    (and a zero fill, if ``make`` does one) is ordered on that stream, and the caching allocator
+    ties the block to it, so the block is not handed to other work until the launch is done."""
+    s = _torch_stream(stream)
+    with torch.cuda.stream(s):
+        return make()
 
 
 def _ptr(t: torch.Tensor | None):
@@ -204,9 +220,10 @@ def _decode(fn: str, desc: PbbDesc, pos, q, k_new, v_new, k_ring, v_ring, out, w
     for n, t in (("k_ring", k_ring), ("v_ring", v_ring)):
         _expect(n, t, ring_shape(desc), desc.torch_dtype)
     if workspace is None:
-        # a fresh zero-filled workspace when the launch needs one (split workgroups); callers
-        # that capture graphs or step in a loop pass their own from alloc_workspace
-        workspace = alloc_workspace(desc, q.device)
+        # a fresh zero-filled workspace when the launch needs one (split workgroups), allocated
+        # and cleared on the launch stream; callers that capture graphs or step in a loop pass
+        # their own from alloc_workspace
+        workspace = _scratch_on(stream, lambda: alloc_workspace(desc, q.device))
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     extra = () if pos_next is None else (_ptr(pos_next),)
     _check(fn, getattr(load_library(), fn)(
@@ -291,8 +308,9 @@ def _backward(fn: str, desc: PbbDesc, q, k, v, out, dout, lse, dq, dk, dv, works
         _expect(name, t, (desc.batch, n, desc.n_kv_heads, desc.head_dim), desc.torch_dtype)
     _expect("lse", lse, (desc.batch, desc.n_q_heads, n), torch.float32)
     if workspace is None:
-        workspace = torch.empty(max(1, backward_workspace_bytes(desc, n)), dtype=torch.uint8,
-                                device=q.device)
+        nbytes = max(1, backward_workspace_bytes(desc, n))
+        workspace = _scratch_on(stream, lambda: torch.empty(nbytes, dtype=torch.uint8,
+                                                            device=q.device))
     ws_bytes = workspace.numel() * workspace.element_size()
     _check(fn, getattr(load_library(), fn)(
         ctypes.byref(desc), int(n), _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(dout), _ptr(lse),
@@ -311,6 +329,3 @@ def swa_backward(desc: PbbDesc, q, k, v, out, dout, lse, dq, dk, dv, workspace=N
     """Sliding-window counterpart of :func:`pbb_backward`."""
     return _backward("swa_backward", desc, q, k, v, out, dout, lse, dq, dk, dv, workspace, stream)
 
-
-def default_scale(head_dim: int) -> float:
-    return 1.0 / math.sqrt(head_dim)
