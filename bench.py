@@ -58,9 +58,9 @@ def _kernel_hash():
     return h.hexdigest()[:16]
 
 
-def _traffic_from_profile(workload_key):
-    """HBM traffic per launch from the committed rocprofv3 counter summary, or None when the
-    kernel sources changed since the counters were taken."""
+def _profile_values(workload_key):
+    """Values of the committed rocprofv3 counter summary of one decode workload, or None when
+    it is missing or the kernel sources changed since the counters were taken."""
     path = os.path.join(ROOT, "profiles", f"decode_bf16_{workload_key}_counters.txt")
     if not os.path.exists(path):
         return None
@@ -69,12 +69,29 @@ def _traffic_from_profile(workload_key):
         for ln in f:
             if ":" in ln:
                 k, v = ln.split(":", 1)
-                vals[k.strip()] = v.strip()
+                vals[k.strip()] = v.strip().split()[0] if v.strip() else ""
     if vals.get("kernel_source_hash") != _kernel_hash():
         return None
+    return vals
+
+
+def _traffic_from_profile(workload_key):
+    """HBM bytes per launch (FETCH_SIZE and WRITE_SIZE, scaled by the copy calibration) from
+    the committed counter summary, or None (see _profile_values)."""
+    vals = _profile_values(workload_key)
     try:
-        return float(vals["hbm_bytes_per_launch_scaled"])
+        return float(vals["hbm_bytes_per_launch_scaled"]) if vals else None
     except (KeyError, ValueError):
+        return None
+
+
+def _traffic_ratio_from_profile(workload_key):
+    """Counter traffic over the algorithmic bytes of the same profiled launches, or None."""
+    vals = _profile_values(workload_key)
+    try:
+        return (float(vals["hbm_bytes_per_launch_scaled"]) /
+                float(vals["algorithmic_bytes_per_launch"])) if vals else None
+    except (KeyError, ValueError, ZeroDivisionError):
         return None
 
 
@@ -120,39 +137,87 @@ class Workload:
         q, k, v = self.inputs[0][i], self.inputs[1][i], self.inputs[2][i]
         self.fn(self.desc, self.pos, q, k, v, self.k_ring, self.v_ring, self.out, self.ws)
 
-    def timed(self, warmup, steps):
-        """Returns (elapsed seconds of the whole loop, mean kernel seconds, algorithmic bytes).
+    def timed(self, warmup, steps, graph=True):
+        """Time ``steps`` decode steps after ``warmup`` untimed ones.  A timed step is one
+        launch: the positions advance on the device inside the decode kernel
+        (``*_decode_step_advance`` writing pos + 1 into a second position buffer, the two
+        buffers alternating), as the paper's decode loop advances them on the device.
 
-        A timed step is one launch: the positions advance on the device inside the decode
-        kernel (``*_decode_step_advance`` writing pos + 1 into a second position buffer, the two
-        buffers alternating), as the paper's decode loop advances them on the device."""
+        Two passes over the same steps from the same state (rings and positions restored from a
+        snapshot taken after the warmup):
+          * eager: back-to-back launches on one stream with HIP events around each launch on
+            that stream -> ``kernel_s``, the mean kernel duration (the roofline's figure);
+          * graph (``graph=True``): the same launches captured as one HIP graph, replayed once
+            untimed and once timed -> ``wall_s``, the wall clock of the whole replay between
+            two synchronisations (the throughput figure), and ``graph_event_s``, HIP events
+            around it.
+        Without ``graph``, ``wall_s`` is the eager loop's wall clock.  ``bytes``: algorithmic
+        bytes of the timed steps (their actual positions)."""
         import torch
         for i in range(warmup):
             self.step(i)
             self.pos += 1
         torch.cuda.synchronize()
-        starts = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
-        ends = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
         total_bytes = 0
         t_first = (self.t0 + warmup)
         for i in range(steps):
             total_bytes += step_bytes(t_first + i, self.cfg)
-        torch.cuda.synchronize()
+        snap = (self.k_ring.clone(), self.v_ring.clone(), self.pos.clone())
         bufs = (self.pos, self.pos_next)
-        w0 = time.perf_counter()
-        for i in range(steps):
+
+        def restore():
+            self.k_ring.copy_(snap[0])
+            self.v_ring.copy_(snap[1])
+            self.pos.copy_(snap[2])
+            torch.cuda.synchronize()
+
+        def launch(i):
             j = warmup + i
-            starts[i].record()
             self.fn_advance(self.desc, bufs[i % 2], bufs[(i + 1) % 2], self.inputs[0][j],
                             self.inputs[1][j], self.inputs[2][j], self.k_ring, self.v_ring,
                             self.out, self.ws)
+
+        res = {"bytes": total_bytes}
+        if graph:
+            restore()
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                for i in range(steps):
+                    launch(i)
+            restore()
+            g.replay()                  # first replay: untimed
+            restore()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            w0 = time.perf_counter()
+            e0.record()
+            g.replay()
+            e1.record()
+            torch.cuda.synchronize()
+            res["wall_s"] = time.perf_counter() - w0
+            res["graph_event_s"] = e0.elapsed_time(e1) / 1e3
+            del g
+        restore()
+        starts = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+        ends = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+        w0 = time.perf_counter()
+        for i in range(steps):
+            starts[i].record()
+            launch(i)
             ends[i].record()
         torch.cuda.synchronize()
-        elapsed = time.perf_counter() - w0
+        res["eager_wall_s"] = time.perf_counter() - w0
         if steps % 2:
             self.pos.copy_(self.pos_next)   # self.pos holds the next position, as after step()
-        kern = sum(s.elapsed_time(e) for s, e in zip(starts, ends)) / 1e3 / steps
-        return elapsed, kern, total_bytes
+        res["kernel_s"] = sum(s.elapsed_time(e) for s, e in zip(starts, ends)) / 1e3 / steps
+        if not graph:
+            res["wall_s"] = res["eager_wall_s"]
+        del snap
+        return res
+
+
+def _tup(res):
+    """(wall seconds, mean kernel seconds, algorithmic bytes) of a Workload.timed result."""
+    return res["wall_s"], res["kernel_s"], res["bytes"]
 
 
 MFMA_BF16_PEAK_TFLOPS = 2500.0
@@ -402,46 +467,173 @@ def paper_latency(device, shapes=(10, 12, 14), origins=(8192,), steps=256, reps=
     return res
 
 
-def cpu_baseline(cfg, t0, device, budget_s=12.0, n_seq=32, min_reps=1, threads=None):
-    """Time the fp64 CPU oracle on the first decode step of the workload's first ``n_seq``
-    sequences, repeating the sample at least ``min_reps`` times and until ``budget_s`` seconds
-    have elapsed."""
+def _host_cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            return next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), "")
+    except OSError:
+        return ""
+
+
+def _bf16_round(x):
+    """float64 -> nearest bfloat16 value, ties to even (8 significant bits)."""
+    import numpy as np
+    out = np.zeros_like(x)
+    nz = x != 0
+    ulp = np.exp2(np.floor(np.log2(np.abs(x[nz]))) - 7)
+    out[nz] = np.round(x[nz] / ulp) * ulp
+    return out
+
+
+def _error_stats(got, ref):
+    """max |got - ref|, max |got - bf16(ref)|, worst relative L2 and cosine per (seq, head)."""
+    import numpy as np
+    g = got.reshape(-1, got.shape[-1]).astype(np.float64)
+    r = ref.reshape(-1, ref.shape[-1])
+    rn = np.linalg.norm(r, axis=1)
+    return {"max_abs": float(np.abs(g - r).max()),
+            "max_abs_vs_bf16_ref": float(np.abs(g - _bf16_round(r)).max()),
+            "rel_l2_max": float((np.linalg.norm(g - r, axis=1) / np.maximum(rn, 1e-30)).max()),
+            "cos_min": float(((g * r).sum(1) / np.maximum(np.linalg.norm(g, axis=1) * rn,
+                                                          1e-30)).min())}
+
+
+def cpu_baseline(cfg, t0, device, budget_s=10.0, max_steps=48, threads=None,
+                 single_thread=True):
+    """The fp64 CPU oracle timed on FULL-BATCH decode steps of the workload: steps 0, 1, 2, ..
+    (every sequence, every query head) with all host threads until ``budget_s`` seconds have
+    passed (at least 3 steps, at most ``max_steps``), then one full-batch step single-threaded.
+    The same steps are also run on the GPU from the same ring state, and the oracle's outputs
+    are compared with them (error statistics, outside the clock)."""
     import numpy as np
     import torch
     import oracle
     import workloads as W
     if threads is None:
         threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or (os.cpu_count() or 1)
-    n = min(n_seq, cfg.batch)
+    n = cfg.batch
     rows = torch.arange(n, dtype=torch.int64)
     back = cfg.slots
-    lo = t0[:n] - back
-    posm = lo.view(-1, 1) + torch.arange(0, back + 1, dtype=torch.int64).view(1, -1)
-    kh = W.kv_at(cfg, "k", rows, posm, device=device).float().cpu().numpy()
-    vh = W.kv_at(cfg, "v", rows, posm, device=device).float().cpu().numpy()
-    q = W.q_at(cfg, t0[:n], device=device).float().cpu().numpy()
+    lo = (t0 - back).numpy()
+    hpos = torch.as_tensor(lo).view(-1, 1) + torch.arange(0, back + max_steps,
+                                                          dtype=torch.int64).view(1, -1)
+    kh = np.empty((n, cfg.hkv, back + max_steps, cfg.d), dtype=np.float32)
+    vh = np.empty_like(kh)
+    for c0 in range(0, n, 32):
+        kh[c0:c0 + 32] = W.kv_at(cfg, "k", rows[c0:c0 + 32], hpos[c0:c0 + 32],
+                                 device=device).float().cpu().numpy()
+        vh[c0:c0 + 32] = W.kv_at(cfg, "v", rows[c0:c0 + 32], hpos[c0:c0 + 32],
+                                 device=device).float().cpu().numpy()
+    # GPU outputs of the same steps from the pre-filled rings
+    wl = Workload(cfg, t0, max_steps, device)
+    gpu_out = []
+    for i in range(max_steps):
+        wl.step(i)
+        wl.pos += 1
+        gpu_out.append(wl.out.float().cpu().numpy())
+    qs = wl.inputs[0].float().cpu().numpy()
+    del wl
+    torch.cuda.empty_cache()
     mode = oracle.SWA if cfg.mode == "swa" else oracle.PBB
-    pos = t0[:n].numpy().astype(np.int64)
-    oracle.decode(mode, pos[:1], q[:1], kh[:1], vh[:1], lo[:1].numpy(), block=cfg.block,
+    t0n = t0.numpy().astype(np.int64)
+    oracle.decode(mode, t0n[:1], qs[0][:1], kh[:1], vh[:1], lo[:1], block=cfg.block,
                   window=cfg.window, n_threads=1)  # load the library outside the clock
-    done, w0 = 0, time.perf_counter()
-    while True:
-        oracle.decode(mode, pos, q, kh, vh, lo.numpy(), block=cfg.block, window=cfg.window,
-                      n_threads=threads)
-        done += n
-        if done >= min_reps * n and time.perf_counter() - w0 >= budget_s:
+    refs = []
+    w0 = time.perf_counter()
+    while len(refs) < max_steps:
+        i = len(refs)
+        refs.append(oracle.decode(mode, t0n + i, qs[i], kh, vh, lo, block=cfg.block,
+                                  window=cfg.window, n_threads=threads))
+        if len(refs) >= 3 and time.perf_counter() - w0 >= budget_s:
             break
     el = time.perf_counter() - w0
-    model = ""
-    try:
-        with open("/proc/cpuinfo") as f:
-            model = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), "")
-    except OSError:
-        pass
-    return {"value": done / el, "unit": "tokens/s", "cores": threads, "kind": "oracle",
-            "sample": f"first decode step of sequences 0..{n - 1} of {cfg.name} (all {cfg.hq} "
-                      f"query heads each), repeated {done // n}x over {el:.1f} s; fp64 C oracle, "
-                      f"{threads} threads; host CPU: {model}"}
+    res = {"value": n * len(refs) / el, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+           "sample": f"{len(refs)} full-batch decode steps of {cfg.name} (all {n} sequences x "
+                     f"{cfg.hq} query heads each, positions t0+0..t0+{len(refs) - 1}) in "
+                     f"{el:.1f} s; fp64 C oracle with {threads} threads on the host CPU "
+                     f"({_host_cpu_model()}, {os.cpu_count()} logical CPUs visible)",
+           "host_cpu": _host_cpu_model()}
+    if single_thread:
+        w0 = time.perf_counter()
+        oracle.decode(mode, t0n, qs[0], kh, vh, lo, block=cfg.block, window=cfg.window,
+                      n_threads=1)
+        res["single_thread_value"] = n / (time.perf_counter() - w0)
+    stats = None
+    for i, ref in enumerate(refs):
+        e = _error_stats(gpu_out[i], ref)
+        stats = e if stats is None else {k: (min(stats[k], e[k]) if k == "cos_min"
+                                             else max(stats[k], e[k])) for k in e}
+    res["gpu_vs_oracle"] = dict(stats, steps=len(refs))
+    return res
+
+
+PROBE_LIB = os.path.join(ROOT, "paper_2606_02680_amd", "libpbbprobe.so")
+
+
+def stream_probe(device, cfg, t0, waves, nontemporal=True, equal=False, reps=10):
+    """Practical read rate of the decode's streaming pattern (include/pbb_probe.h): every
+    (sequence, KV head) unit of ``cfg`` reads its K and V rows through LDS DMA, two 32-row steps
+    in flight per wave, ``waves`` waves per unit, no arithmetic.  Rows per unit: the support's
+    ring rows at positions ``t0`` (|A(t)| - 1, the decode's ragged sizes), or the whole ring
+    minus one row with ``equal``.  Returns GB/s (rows actually read / median launch time from
+    HIP events on the launch stream) and the bytes per launch."""
+    import ctypes
+    import torch
+    if not os.path.exists(PROBE_LIB):
+        raise ImportError(f"{PROBE_LIB} not found: build it with `python -m paper_2606_02680_amd.build`")
+    lib = ctypes.CDLL(PROBE_LIB)
+    vp = ctypes.c_void_p
+    lib.pbb_probe_stream.argtypes = [vp, vp, ctypes.c_size_t, vp, ctypes.c_int32, ctypes.c_int32,
+                                     ctypes.c_int32, ctypes.c_int32, vp, vp]
+    lib.pbb_probe_stream.restype = ctypes.c_int
+    assert cfg.d == 128 and cfg.dtype == "bf16"
+    units, slots = cfg.batch * cfg.hkv, cfg.slots
+    k = torch.empty(units * slots * 128, dtype=torch.bfloat16, device=device)
+    v = torch.empty_like(k)
+    per_seq = (torch.full_like(t0, slots - 1) if equal else support_size(t0, cfg) - 1)
+    rows = per_seq.view(-1, 1).expand(-1, cfg.hkv).reshape(-1).to(torch.int32).to(device)
+    sink = torch.zeros(1, dtype=torch.float32, device=device)
+    stream = torch.cuda.current_stream()
+
+    def launch():
+        rc = lib.pbb_probe_stream(vp(k.data_ptr()), vp(v.data_ptr()), ctypes.c_size_t(slots * 256),
+                                  vp(rows.data_ptr()), units, slots, waves, int(nontemporal),
+                                  vp(sink.data_ptr()), vp(stream.cuda_stream))
+        if rc != 0:
+            raise RuntimeError(f"pbb_probe_stream failed ({rc})")
+
+    for _ in range(2):
+        launch()
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(reps)]
+    for e0, e1 in ev:
+        e0.record(stream)
+        launch()
+        e1.record(stream)
+    torch.cuda.synchronize()
+    ms = sorted(e0.elapsed_time(e1) for e0, e1 in ev)[reps // 2]
+    nbytes = 2 * 256 * int(rows.to(torch.int64).sum())
+    del k, v
+    torch.cuda.empty_cache()
+    return {"gbps": nbytes / (ms * 1e-3) / 1e9, "bytes_per_launch": nbytes, "us": ms * 1e3,
+            "waves": waves, "nontemporal": bool(nontemporal),
+            "rows": "whole ring" if equal else "support (ragged)"}
+
+
+def stream_probes(device, steps_offset=0):
+    """The probe at the decode workloads' shapes and launch shapes (c3, c4; c5's equal rows)."""
+    import workloads as W
+    res = {}
+    c3, c4, c5 = W.get_config("c3"), W.get_config("c4"), W.get_config("c5")
+    t3 = W.initial_positions(c3) + steps_offset
+    t4 = W.initial_positions(c4) + steps_offset
+    res["c3_ragged_nw4"] = stream_probe(device, c3, t3, 4)
+    res["c3_equal_nw4"] = stream_probe(device, c3, t3, 4, equal=True)
+    res["c4_ragged_nw2"] = stream_probe(device, c4, t4, 2)
+    res["c4_ragged_nw4"] = stream_probe(device, c4, t4, 4)
+    res["c5_equal_nw4"] = stream_probe(device, c5, t3, 4, equal=True)
+    return res
 
 
 def copy_ceiling(device, reps=5):
@@ -494,9 +686,8 @@ def oracle_all_steps(cfg, device, threads=None):
 
 
 def oracle_timing(device):
-    """The fp64 CPU oracle: every step of c1 and c2, and on full batches the first decode step
-    of every sequence of c3, c4 and c5, at least three times and 5 s each with all host
-    threads, and once single-threaded (c3)."""
+    """The fp64 CPU oracle: every step of c1 and c2, and full-batch decode steps of c3, c4 and
+    c5 (at least three and 5 s each with all host threads, plus one single-threaded step)."""
     import workloads as W
     res = {"host_threads": os.cpu_count()}
     for name in ("c1", "c2"):
@@ -504,10 +695,7 @@ def oracle_timing(device):
     for name in ("c3", "c4", "c5"):
         cfg = W.get_config(name)
         t0 = W.initial_positions(cfg)
-        res[name] = cpu_baseline(cfg, t0, device, budget_s=5.0, n_seq=cfg.batch, min_reps=3)
-    cfg = W.get_config("c3")
-    res["c3_single_thread"] = cpu_baseline(cfg, W.initial_positions(cfg), device, budget_s=0.0,
-                                           n_seq=cfg.batch, min_reps=1, threads=1)
+        res[name] = cpu_baseline(cfg, t0, device, budget_s=5.0)
     return res
 
 
@@ -537,6 +725,13 @@ def main(argv=None):
                     help="only time the CPU oracle (all steps of c1, c2; full batches of c3, c4, c5; minutes)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only time a plain 1 GiB device copy (HBM counter calibration)")
+    ap.add_argument("--stream-probe", action="store_true",
+                    help="only run the LDS-DMA streaming-read probe at the decode workloads' "
+                         "shapes (the practical read ceiling)")
+    ap.add_argument("--records", default=None,
+                    help="also write one JSON record per measured workload to this file")
+    ap.add_argument("--no-graph", action="store_true",
+                    help="time the steps as eager back-to-back launches instead of a HIP graph")
     args = ap.parse_args(argv)
     if args.gpus != 1:
         print(f"bench.py: this build measures one GPU only; --gpus {args.gpus} is not supported "
@@ -571,6 +766,10 @@ def main(argv=None):
         print(json.dumps({"prefill": prefill_extras(device)}), flush=True)
         return 0
 
+    if args.stream_probe:
+        print(json.dumps({"stream_probe": stream_probes(device)}), flush=True)
+        return 0
+
     if args.oracle_timing:
         print(json.dumps({"oracle_timing": oracle_timing(device)}), flush=True)
         return 0
@@ -589,7 +788,7 @@ def main(argv=None):
         for name, over in (("c3", {}), ("c4", {}), ("c3", {"hq": 8}), ("c4", {"hq": 2, "batch": 512})):
             c = W.get_config(name).with_(dtype="f32", **over)
             wl = Workload(c, W.initial_positions(c), 60, device)
-            el, ks, tb = wl.timed(10, 50)
+            el, ks, tb = _tup(wl.timed(10, 50))
             key = f"{name}_shapes_fp32_G{c.hq // c.hkv}_batch{c.batch}"
             res[key] = {"kernel_us": ks * 1e6, "tokens_per_s": c.batch * 50 / el,
                         "hbm_gbps_kernel": tb / 50 / ks / 1e9,
@@ -605,7 +804,7 @@ def main(argv=None):
         for batch in (16, 32, 64, 128, 256, 512, 1024):
             c = W.get_config("c3").with_(batch=batch)
             wl = Workload(c, W.initial_positions(c), 60, device)
-            el, ks, tb = wl.timed(10, 50)
+            el, ks, tb = _tup(wl.timed(10, 50))
             res[f"batch{batch}"] = {"kernel_us": ks * 1e6, "tokens_per_s": batch * 50 / el,
                                     "hbm_gbps_kernel": tb / 50 / ks / 1e9,
                                     "frac_of_peak": tb / 50 / ks / 1e9 / HBM_PEAK_GBPS,
@@ -626,7 +825,8 @@ def main(argv=None):
     t0 = W.initial_positions(cfg)
     print(f"[bench] preparing {cfg.name} ({n_steps} steps of inputs)", file=sys.stderr, flush=True)
     wl = Workload(cfg, t0, n_steps, device)
-    elapsed, kern_s, total_bytes = wl.timed(args.warmup, args.steps)
+    tm = wl.timed(args.warmup, args.steps, graph=not args.no_graph)
+    elapsed, kern_s, total_bytes = tm["wall_s"], tm["kernel_s"], tm["bytes"]
     tokens = cfg.batch * args.steps
     value = tokens / elapsed
     achieved = total_bytes / args.steps / kern_s / 1e9
@@ -649,13 +849,21 @@ def main(argv=None):
                    "batch": cfg.batch, "n_q_heads": cfg.hq, "n_kv_heads": cfg.hkv,
                    "head_dim": cfg.d, "block": cfg.block, "slots": cfg.slots,
                    "window": cfg.window, "parallelism": "single GPU"},
+        "timing": ("steps captured as one HIP graph (one launch per step, positions advanced on "
+                   "the device), wall clock of the replay; kernel time from a second, eager pass "
+                   "over the same steps with HIP events around each launch"
+                   if not args.no_graph else
+                   "eager back-to-back launches with HIP events around each launch"),
         "hbm_gbps_step": total_bytes / elapsed / 1e9,
         "bytes_per_token": total_bytes / tokens,
         "kernel_us": kern_s * 1e6,
+        "eager_ms_per_step": tm["eager_wall_s"] / args.steps * 1e3,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS,
                      "traffic": _traffic_from_profile(args.config)},
     }
+    if "graph_event_s" in tm:
+        result["graph_event_us_per_step"] = tm["graph_event_s"] / args.steps * 1e6
     print(f"[bench] {cfg.name}: {value:.4g} tokens/s, kernel {kern_s * 1e6:.1f} us, "
           f"{achieved:.1f} GB/s", file=sys.stderr, flush=True)
 
@@ -673,17 +881,21 @@ def main(argv=None):
                         ("swa_ring_w2048_s2048", W.get_config("c5").with_(window=2048,
                                                                           slots=2048))):
             sw = Workload(c, t0, n_steps, device, inputs=inputs)
-            el, ks, tb = sw.timed(args.warmup, ext_steps)
+            el, ks, tb = _tup(sw.timed(args.warmup, ext_steps))
             extra[name] = {"tokens_per_s": cfg.batch * ext_steps / el, "kernel_us": ks * 1e6,
                            "bytes_per_token": tb / (cfg.batch * ext_steps),
                            "hbm_gbps_kernel": tb / ext_steps / ks / 1e9,
+                           "frac_of_peak": tb / ext_steps / ks / 1e9 / HBM_PEAK_GBPS,
                            "pbb_over_swa_tokens_per_s": value / (cfg.batch * ext_steps / el)}
+            if name == "swa_ring_w4096_s4096":
+                extra[name]["traffic"] = _traffic_from_profile("c5")
+                extra[name]["traffic_over_algorithmic"] = _traffic_ratio_from_profile("c5")
             del sw
             torch.cuda.empty_cache()
         # The same step with the rotary embedding fused in (q and the new key turned by position,
         # base 10^6): timing only, so the pre-filled ring is not re-rotated.
         rw = Workload(cfg.with_(rope_base=1e6), t0, n_steps, device, inputs=inputs)
-        el, ks, tb = rw.timed(args.warmup, ext_steps)
+        el, ks, tb = _tup(rw.timed(args.warmup, ext_steps))
         extra["c3_rope_base1e6"] = {"tokens_per_s": cfg.batch * ext_steps / el,
                                     "kernel_us": ks * 1e6,
                                     "hbm_gbps_kernel": tb / ext_steps / ks / 1e9,
@@ -694,12 +906,14 @@ def main(argv=None):
         c4 = W.get_config("c4")
         t4 = W.initial_positions(c4)
         w4 = Workload(c4, t4, args.warmup + ext_steps, device)
-        el, ks, tb = w4.timed(args.warmup, ext_steps)
+        el, ks, tb = _tup(w4.timed(args.warmup, ext_steps))
         extra["c4_ragged_gqa8"] = {"tokens_per_s": c4.batch * ext_steps / el,
                                    "kernel_us": ks * 1e6,
                                    "bytes_per_token": tb / (c4.batch * ext_steps),
                                    "hbm_gbps_kernel": tb / ext_steps / ks / 1e9,
-                                   "frac_of_peak": tb / ext_steps / ks / 1e9 / HBM_PEAK_GBPS}
+                                   "frac_of_peak": tb / ext_steps / ks / 1e9 / HBM_PEAK_GBPS,
+                                   "traffic": _traffic_from_profile("c4"),
+                                   "traffic_over_algorithmic": _traffic_ratio_from_profile("c4")}
         del w4
         torch.cuda.empty_cache()
         extra["paper_shape_latency_us_per_step"] = paper_latency(
@@ -708,8 +922,14 @@ def main(argv=None):
         extra["prefill"] = prefill_extras(device)
         extra["backward"] = backward_extras(device)
         copy_gbps = copy_ceiling(device)
-        extra["hbm_copy_ceiling"] = {"copy_gbps_read_plus_write": copy_gbps,
-                                     "graded_kernel_frac_of_copy": achieved / copy_gbps}
+        probes = stream_probes(device, steps_offset=args.warmup)
+        extra["hbm_copy_ceiling"] = {
+            "copy_gbps_read_plus_write": copy_gbps,
+            "graded_kernel_frac_of_copy": achieved / copy_gbps,
+            "stream_probe": probes,
+            "graded_kernel_frac_of_stream_probe": achieved / probes["c3_ragged_nw4"]["gbps"],
+            "c4_kernel_frac_of_stream_probe": (extra["c4_ragged_gqa8"]["hbm_gbps_kernel"] /
+                                               probes["c4_ragged_nw2"]["gbps"])}
         result["extra"] = extra
         result["paper_context"] = ("Flash-PBB 1.82x Flash-SWA decode-core throughput on an RTX "
                                    "4090 (48 GB), BF16, batch 1, Hkv 2, d 64, b 128 vs w 128")
@@ -717,8 +937,40 @@ def main(argv=None):
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
         result["cpu_baseline"] = cpu_baseline(cfg, t0, device)
+    if args.records:
+        write_records(args.records, result)
     print(json.dumps(result), flush=True)
     return 0
+
+
+def write_records(path, result):
+    """One JSON record per measured workload: throughput, time per step, bytes per token,
+    achieved rate against 8 TB/s and the streaming probe, counter traffic where a committed
+    summary matches the kernel, and the oracle comparison of the CPU-baseline leg."""
+    extra = result.get("extra", {})
+    probe = extra.get("hbm_copy_ceiling", {}).get("stream_probe", {})
+    recs = [{"workload": result["config"]["workload"], "tokens_per_s": result["value"],
+             "us_per_step": result["ms_per_step"] * 1e3, "kernel_us": result["kernel_us"],
+             "bytes_per_token": result["bytes_per_token"],
+             "gbps_kernel": result["roofline"]["achieved"],
+             "frac_of_8tbps": result["roofline"]["frac"],
+             "frac_of_stream_probe": (result["roofline"]["achieved"] /
+                                      probe["c3_ragged_nw4"]["gbps"]) if probe else None,
+             "traffic_bytes_per_launch": result["roofline"]["traffic"],
+             "gpu_vs_oracle": result.get("cpu_baseline", {}).get("gpu_vs_oracle"),
+             "oracle_tokens_per_s": result.get("cpu_baseline", {}).get("value")}]
+    for name in ("swa_ring_w4096_s4096", "swa_ring_w2048_s4096", "swa_ring_w2048_s2048",
+                 "c3_rope_base1e6", "c4_ragged_gqa8"):
+        if name in extra:
+            recs.append({"workload": name, **extra[name]})
+    for group in ("prefill", "backward"):
+        for name, r in extra.get(group, {}).items():
+            recs.append({"workload": name, **r})
+    for name, r in extra.get("paper_shape_latency_us_per_step", {}).items():
+        recs.append({"workload": f"paper_shape_{name}", **r})
+    with open(path, "w") as f:
+        for r in recs:
+            f.write(json.dumps(r) + "\n")
 
 
 if __name__ == "__main__":

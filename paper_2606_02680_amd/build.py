@@ -2,8 +2,11 @@
 
 ``python -m paper_2606_02680_amd.build`` compiles ``csrc/pbb_api.cpp``,
 ``csrc/pbb_kernels.hip`` (decode), ``csrc/pbb_prefill.hip`` (prefill) and
-``csrc/pbb_backward.hip`` (training backward) into ``paper_2606_02680_amd/libpbb.so`` and writes the compiler's
-per-kernel resource report (VGPRs, AGPRs, SGPRs, LDS, scratch) to ``csrc/resource_usage.txt``.
+``csrc/pbb_backward.hip`` (training backward) into ``paper_2606_02680_amd/libpbb.so`` (and the
+streaming-read probe ``csrc/pbb_probe.hip``, a measurement helper, into ``libpbbprobe.so``) and
+writes the compiler's
+per-kernel resource report (VGPRs, AGPRs, SGPRs, LDS, scratch) to ``_build/resource_usage.txt``
+(an untracked build output next to the library).
 """
 from __future__ import annotations
 
@@ -15,6 +18,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libpbb.so")
+PROBE_LIB = os.path.join(PKG, "libpbbprobe.so")   # measurement helper (include/pbb_probe.h)
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [
@@ -45,12 +49,26 @@ def build(verbose: bool = False) -> str:
         sys.stderr.write("\n".join(other) + "\n")
         raise RuntimeError(f"hipcc failed ({proc.returncode}): {' '.join(cmd)}")
     os.replace(tmp, LIB)
-    with open(os.path.join(CSRC, "resource_usage.txt"), "w") as f:
+    os.makedirs(os.path.join(PKG, "_build"), exist_ok=True)
+    with open(os.path.join(PKG, "_build", "resource_usage.txt"), "w") as f:
         for ln in report:
             f.write(ln.split("remark: ", 1)[-1].strip() + "\n")
     if verbose and other:
         print("\n".join(other))
+    build_probe()
     return LIB
+
+
+def build_probe() -> str:
+    """Compile the streaming-read probe (``csrc/pbb_probe.hip``) into ``libpbbprobe.so``."""
+    tmp = PROBE_LIB + ".tmp"
+    cmd = [hipcc(), *HIPCC_FLAGS, os.path.join(CSRC, "pbb_probe.hip"), "-o", tmp]
+    proc = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
+    if proc.returncode != 0:
+        sys.stderr.write(proc.stdout + "\n")
+        raise RuntimeError(f"hipcc failed ({proc.returncode}): {' '.join(cmd)}")
+    os.replace(tmp, PROBE_LIB)
+    return PROBE_LIB
 
 
 if __name__ == "__main__":

@@ -304,3 +304,29 @@ def test_split_rule_over_random_descriptors():
         counters = -(-(units * 4) // 256) * 256
         part = units * S * G * (d + 2) * 4
         assert got == counters + -(-part // 256) * 256, (batch, hkv, G, d, swa, span)
+
+
+def test_stream_probe_library_exports_and_validates():
+    """The measurement helper libpbbprobe.so exports what include/pbb_probe.h declares and
+    rejects bad arguments on the host (code 1) before any HIP call."""
+    path = os.path.join(os.path.dirname(B._LIB_PATH), "libpbbprobe.so")
+    lib = ctypes.CDLL(path)
+    text = open(os.path.join(os.path.dirname(HEADER), "pbb_probe.h")).read()
+    names = set(re.findall(r"^\S.*?\b(pbb_probe_[a-z_]+)\s*\(", text, re.M))
+    assert names == {"pbb_probe_stream"}
+    vp = ctypes.c_void_p
+    f = lib.pbb_probe_stream
+    f.argtypes = [vp, vp, ctypes.c_size_t, vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                  ctypes.c_int32, vp, vp]
+    f.restype = ctypes.c_int
+    ok = dict(k=A, v=A, stride=2048 * 256, rows=A, units=4, max_rows=2048, waves=4, nt=1, sink=A)
+
+    def call(**kw):
+        a = dict(ok, **kw)
+        return f(vp(a["k"]), vp(a["v"]), ctypes.c_size_t(a["stride"]), vp(a["rows"]), a["units"],
+                 a["max_rows"], a["waves"], a["nt"], vp(a["sink"]), vp(0))
+
+    assert call(k=0) == 1 and call(rows=0) == 1 and call(sink=0) == 1
+    assert call(units=0) == 1 and call(waves=3) == 1 and call(max_rows=0) == 1
+    assert call(max_rows=2049) == 1          # rows would run past the unit's region
+    assert call(k=A + 8) == 1 and call(stride=2048 * 256 + 8) == 1
