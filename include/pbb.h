@@ -182,6 +182,25 @@ pbb_status_t swa_decode_step_advance(const pbb_desc_t *desc, const int32_t *pos,
                                      size_t workspace_bytes, void *stream);
 
 /*
+ * pbb_decode_step for callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the same step, with no
+ * workspace argument.  When the launch needs a workspace (split launches: bf16, at most 64
+ * (sequence, KV head) units, block above 256), it uses a buffer the library holds per device
+ * -- PBB_NOALLOC_SCRATCH_BYTES bytes in a static device array, resolved on the first call on
+ * each device (which also clears its counters with a fill kernel on `stream`, so a capture of
+ * that first call records the clear) and kept until the process ends.  Never calls hipMalloc,
+ * hipFree or an allocating routine.  Calls whose workspace would exceed that size return
+ * PBB_ERR_WORKSPACE and enqueue nothing; every decode descriptor the library accepts fits.
+ * Every call on one device shares the buffer and leaves its counters zero: calls that may
+ * overlap on one GPU (other streams, other host threads) race and must be serialised by the
+ * caller.  The stream must belong to the current HIP device.
+ */
+#define PBB_NOALLOC_SCRATCH_BYTES 4260096u
+pbb_status_t pbb_decode_step_noalloc(const pbb_desc_t *desc, const int32_t *pos, const void *q,
+                                     const void *k_new, const void *v_new, void *k_ring,
+                                     void *v_ring, void *out, void *stream);
+
+/*
  * Prefill: attention for every position of prompts at positions 0..n-1, the step that fills
  * the cache before decoding (Sec. 3: one fused kernel over block tiles and bridge rectangles
  * with log-sum-exp rescaling and native GQA; Appendix F.4: the added edges are h x h

@@ -14,6 +14,9 @@
 
 namespace {
 
+static_assert(PBB_NOALLOC_SCRATCH_BYTES == pbb::kNoAllocScratchBytes,
+              "the public scratch size must match the library's buffer");
+
 using pbb::kMaxGroup;
 using pbb::kSplitMaxUnits;
 using pbb::kSplitMaxWays;
@@ -81,10 +84,12 @@ size_t decode_workspace(const pbb_desc_t* d, bool swa) {
   return counters_bytes(d) + (part + 255) / 256 * 256;
 }
 
+// `use_scratch`: the workspace, when the launch needs one, is the library's per-device scratch
+// buffer (the allocation-free entry point) instead of the caller's.
 pbb_status_t decode_common(const pbb_desc_t* desc, bool swa, const int32_t* pos, int32_t* pos_next,
                            bool want_next, const void* q, const void* k_new, const void* v_new,
                            void* k_ring, void* v_ring, void* out, void* workspace,
-                           size_t workspace_bytes, void* stream) {
+                           size_t workspace_bytes, void* stream, bool use_scratch = false) {
   const pbb_status_t st = check_desc(desc, swa);
   if (st != PBB_OK) return st;
   if (!pos || !q || !k_new || !v_new || !k_ring || !v_ring || !out) return PBB_ERR_NULL;
@@ -98,6 +103,15 @@ pbb_status_t decode_common(const pbb_desc_t* desc, bool swa, const int32_t* pos,
       !aligned(k_ring, 16) || !aligned(v_ring, 16) || !aligned(out, 16))
     return PBB_ERR_ALIGN;
   const size_t need = decode_workspace(desc, swa);
+  if (use_scratch) {
+    if (need > pbb::kNoAllocScratchBytes) return PBB_ERR_WORKSPACE;
+    if (desc->rope_base > 0.0f && desc->dtype != PBB_DTYPE_BF16) return PBB_ERR_DTYPE;
+    if (need > 0) {
+      if (pbb::noalloc_scratch(&workspace, reinterpret_cast<hipStream_t>(stream)) != hipSuccess)
+        return PBB_ERR_LAUNCH;
+      workspace_bytes = pbb::kNoAllocScratchBytes;
+    }
+  }
   if (need > 0 && (workspace == nullptr || workspace_bytes < need)) return PBB_ERR_WORKSPACE;
   if (need > 0 && !aligned(workspace, 16)) return PBB_ERR_ALIGN;
 
@@ -328,6 +342,13 @@ pbb_status_t swa_decode_step(const pbb_desc_t* desc, const int32_t* pos, const v
                              void* out, void* workspace, size_t workspace_bytes, void* stream) {
   return decode_common(desc, true, pos, nullptr, false, q, k_new, v_new, k_ring, v_ring, out,
                        workspace, workspace_bytes, stream);
+}
+
+pbb_status_t pbb_decode_step_noalloc(const pbb_desc_t* desc, const int32_t* pos, const void* q,
+                                     const void* k_new, const void* v_new, void* k_ring,
+                                     void* v_ring, void* out, void* stream) {
+  return decode_common(desc, false, pos, nullptr, false, q, k_new, v_new, k_ring, v_ring, out,
+                       nullptr, 0, stream, true);
 }
 
 pbb_status_t pbb_decode_step_advance(const pbb_desc_t* desc, const int32_t* pos, int32_t* pos_next,

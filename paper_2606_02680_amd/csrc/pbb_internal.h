@@ -18,6 +18,13 @@ constexpr int32_t kMaxGroup = 16;         // query heads per KV head held by one
 constexpr int64_t kSplitMaxUnits = 64;    // bf16 decode launches with at most this many units split
 constexpr int64_t kSplitMaxWays = 8;      // workgroups per unit of a split launch, at most
 
+// Largest workspace a decode launch can need: the 256-byte counter block of at most
+// kSplitMaxUnits units, then their partial states (kSplitMaxWays splits x kMaxGroup heads x
+// (head_dim 128 + maximum + sum) floats each) -- 4,260,096 bytes.  The allocation-free entry
+// point keeps one buffer of this size per device.
+constexpr size_t kNoAllocScratchBytes =
+    256 + (size_t)kSplitMaxUnits * kSplitMaxWays * kMaxGroup * (128 + 2) * 4;
+
 // Everything a decode kernel needs, validated on the host before launch.
 struct DecodeArgs {
   const int32_t* pos;
@@ -113,5 +120,10 @@ hipError_t launch_backward_bf16(const BackwardArgs& a, int32_t head_dim, hipStre
 
 // fp32 decode on vector ALUs; head_dim 64 or 128.
 hipError_t launch_decode_f32(const DecodeArgs& a, int32_t head_dim, hipStream_t stream);
+
+// The library-held decode workspace of the current device (kNoAllocScratchBytes bytes): its
+// device address, resolved once per device, whose first call also clears the counter block
+// with a fill kernel on `stream`.  Allocates nothing.
+hipError_t noalloc_scratch(void** ptr, hipStream_t stream);
 
 }  // namespace pbb

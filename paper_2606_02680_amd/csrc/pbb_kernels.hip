@@ -18,14 +18,26 @@
 // log2(e), with a running maximum (online softmax) and fp32 accumulation (Eq.(attention)).
 
 #include <hip/hip_runtime.h>
+#include <mutex>
 #include <type_traits>
 #include <stdint.h>
 
 #include "pbb_device.h"
 #include "pbb_internal.h"
 
+// Decode workspace of the allocation-free entry point (pbb_decode_step_noalloc): the unit
+// counters and partial states of split launches, one copy per device, held until the process
+// ends.  Host code never uses this name as an address: noalloc_scratch() below resolves the
+// device address once per device and every kernel argument uses that.
+static __device__ __align__(256) unsigned char scratch[pbb::kNoAllocScratchBytes];
+
 namespace pbb {
 namespace {
+
+__global__ void scratch_clear_kernel(uint4* __restrict__ p, size_t n16) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n16) p[i] = make_uint4(0u, 0u, 0u, 0u);
+}
 
 // Ring-key ranges of one (sequence, KV head) at position t.
 struct Ranges {
@@ -987,6 +999,32 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
 
 // ------------------------------------------------------------------------------------------
 // Launchers
+
+hipError_t noalloc_scratch(void** ptr, hipStream_t stream) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (addr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    // The unit counters must start at zero (every split launch leaves them zero again); the
+    // block is cleared by a fill kernel, which a graph capture may record.
+    hipLaunchKernelGGL(scratch_clear_kernel, dim3(1), dim3(64), 0, stream, (uint4*)p,
+                       (size_t)(256 / 16));
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    addr[dev] = p;
+  }
+  *ptr = addr[dev];
+  return hipSuccess;
+}
 
 hipError_t launch_ring_zero(void* k_ring, void* v_ring, size_t bytes, hipStream_t stream) {
   const size_t n16 = bytes / 16;

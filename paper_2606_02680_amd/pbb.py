@@ -24,7 +24,8 @@ _TORCH_DTYPE = {DTYPE_F32: torch.float32, DTYPE_BF16: torch.bfloat16}
 EXPORTS = ("pbb_status_string", "pbb_ring_bytes", "pbb_ring_init", "pbb_ring_fill",
            "pbb_workspace_bytes", "pbb_decode_step", "swa_workspace_bytes", "swa_decode_step",
            "pbb_decode_step_advance", "swa_decode_step_advance", "pbb_prefill", "swa_prefill",
-           "pbb_backward_workspace_bytes", "pbb_backward", "swa_backward")
+           "pbb_backward_workspace_bytes", "pbb_backward", "swa_backward",
+           "pbb_decode_step_noalloc")
 
 
 class PbbError(RuntimeError):
@@ -75,6 +76,7 @@ def load_library(path: str = _LIB_PATH):
         getattr(lib, fn).argtypes = [dp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     for fn in ("pbb_decode_step_advance", "swa_decode_step_advance"):
         getattr(lib, fn).argtypes = [dp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.pbb_decode_step_noalloc.argtypes = [dp, vp, vp, vp, vp, vp, vp, vp, vp]
     for fn in ("pbb_prefill", "swa_prefill"):
         getattr(lib, fn).argtypes = [dp, i32, vp, vp, vp, vp, vp, vp, vp, vp]
     lib.pbb_backward_workspace_bytes.argtypes = [dp, i32, ctypes.POINTER(sz)]
@@ -244,6 +246,22 @@ def swa_decode_step(desc: PbbDesc, pos, q, k_new, v_new, k_ring, v_ring, out, wo
     """Fused ring append + sliding-window attention (baseline, same kernels)."""
     return _decode("swa_decode_step", desc, pos, q, k_new, v_new, k_ring, v_ring, out, workspace,
                    stream)
+
+
+def pbb_decode_step_noalloc(desc: PbbDesc, pos, q, k_new, v_new, k_ring, v_ring, out, stream=None):
+    """:func:`pbb_decode_step` without a workspace argument: split launches use the library's
+    per-device scratch buffer (nothing is allocated; overlapping calls on one GPU race)."""
+    _expect("pos", pos, (desc.batch,), torch.int32)
+    _expect("q", q, (desc.batch, desc.n_q_heads, desc.head_dim), desc.torch_dtype)
+    _expect("out", out, (desc.batch, desc.n_q_heads, desc.head_dim), desc.torch_dtype)
+    for n, t in (("k_new", k_new), ("v_new", v_new)):
+        _expect(n, t, (desc.batch, desc.n_kv_heads, desc.head_dim), desc.torch_dtype)
+    for n, t in (("k_ring", k_ring), ("v_ring", v_ring)):
+        _expect(n, t, ring_shape(desc), desc.torch_dtype)
+    _check("pbb_decode_step_noalloc", load_library().pbb_decode_step_noalloc(
+        ctypes.byref(desc), _ptr(pos), _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(k_ring),
+        _ptr(v_ring), _ptr(out), _stream(stream)))
+    return out
 
 
 def pbb_decode_step_advance(desc: PbbDesc, pos, pos_next, q, k_new, v_new, k_ring, v_ring, out,

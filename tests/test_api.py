@@ -306,6 +306,33 @@ def test_split_rule_over_random_descriptors():
         assert got == counters + -(-part // 256) * 256, (batch, hkv, G, d, swa, span)
 
 
+def _noalloc(desc, **ptrs):
+    args = dict(pos=A, q=A, k_new=A, v_new=A, k_ring=A, v_ring=A, out=A)
+    args.update(ptrs)
+    vp = ctypes.c_void_p
+    d = None if desc is None else ctypes.byref(desc)
+    return B.load_library().pbb_decode_step_noalloc(
+        d, vp(args["pos"]), vp(args["q"]), vp(args["k_new"]), vp(args["v_new"]),
+        vp(args["k_ring"]), vp(args["v_ring"]), vp(args["out"]), vp(0))
+
+
+def test_noalloc_argument_errors():
+    """The allocation-free decode validates like pbb_decode_step before touching its scratch
+    buffer (these calls fail before any HIP call, so they run without a GPU)."""
+    assert _noalloc(None) == 1
+    desc = _desc()
+    for name in ("pos", "q", "k_new", "v_new", "k_ring", "v_ring", "out"):
+        assert _noalloc(desc, **{name: 0}) == 1, name
+    assert _noalloc(_desc(block=63, slots=63)) == 2
+    assert _noalloc(_desc(window=64, slots=128, block=64)) == 2   # slots != block (PBB rules)
+    assert _noalloc(_desc(dtype=7)) == 3
+    assert _noalloc(_desc(dtype=B.DTYPE_F32, rope_base=1e6)) == 3
+    assert _noalloc(desc, q=A + 8) == 4
+    # the largest split launch the rules allow fits the library's buffer
+    big = _desc(batch=4, n_q_heads=256, n_kv_heads=16, head_dim=128, block=65536, slots=65536)
+    assert B.workspace_bytes(big) <= 4260096
+
+
 def test_stream_probe_library_exports_and_validates():
     """The measurement helper libpbbprobe.so exports what include/pbb_probe.h declares and
     rejects bad arguments on the host (code 1) before any HIP call."""
