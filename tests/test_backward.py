@@ -57,10 +57,10 @@ def _grad_ok(name, got, ref, bound, heads_axis=2):
     return worst
 
 
-def _check_all(name, mode, inputs, got, ref, block, window):
+def _check_all(name, mode, inputs, got, ref, block, window, scale=None):
     """grad_bounds + _grad_ok for (dq, dk, dv); prints the worst error / allowance ratio."""
     q, k, v, dout, out, lse = inputs
-    bounds = grad_bounds(mode, q, k, v, dout, out, lse, block=block, window=window)
+    bounds = grad_bounds(mode, q, k, v, dout, out, lse, block=block, window=window, scale=scale)
     worst = max(_grad_ok(f"{name} {nm}", g, r, bd)
                 for nm, g, r, bd in zip(("dq", "dk", "dv"), got, ref, bounds))
     print(f"[backward] {name}: largest error / derived allowance {worst:.3f}", flush=True)

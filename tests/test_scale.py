@@ -80,6 +80,7 @@ def test_prefill_and_backward_with_explicit_scale(cuda, mode, n, hq, hkv, d, B, 
     assert np.abs(to_np(lse) - ref_lse).max() <= 2e-3
     rq, rk, rv = oracle.backward(m, to_np(q), to_np(k), to_np(v), to_np(dout), block=cfg.block,
                                  window=cfg.window, scale=scale)
-    from tests.test_backward import _grad_ok
-    for name, g, r in (("dq", dq, rq), ("dk", dk, rk), ("dv", dv, rv)):
-        _grad_ok(f"{mode} scale {scale} {name}", to_np(g), r)
+    from tests.test_backward import _check_all
+    inputs = (to_np(q), to_np(k), to_np(v), to_np(dout), to_np(out), lse.cpu().numpy())
+    _check_all(f"{mode} scale {scale}", mode, inputs, (to_np(dq), to_np(dk), to_np(dv)),
+               (rq, rk, rv), cfg.block, cfg.window, scale=scale)

@@ -135,7 +135,7 @@ def test_prefill_sweep(cuda, i, mode, d, G, hkv, batch, n_pos, block, window):
 
 @pytest.mark.parametrize("i,mode,d,G,hkv,batch,n_pos,block,window", _prompt_cases(8, seed=11))
 def test_backward_sweep(cuda, i, mode, d, G, hkv, batch, n_pos, block, window):
-    from tests.test_backward import _grad_ok
+    from tests.test_backward import _check_all
     cfg, desc, q, k, v = _prompt(i, mode, d, G, hkv, batch, n_pos, block, window, cuda, 500 + i)
     dout, _, _ = W.prompt(cfg.with_(seed=700 + i), n_pos, device=cuda)
     out = torch.empty_like(q)
@@ -149,5 +149,6 @@ def test_backward_sweep(cuda, i, mode, d, G, hkv, batch, n_pos, block, window):
     m = oracle.PBB if mode == "pbb" else oracle.SWA
     rq, rk, rv = oracle.backward(m, to_np(q), to_np(k), to_np(v), to_np(dout), block=block,
                                  window=window)
-    for name, g, r in (("dq", dq, rq), ("dk", dk, rk), ("dv", dv, rv)):
-        _grad_ok(f"backward sweep {i} {name}", to_np(g), r)
+    inputs = (to_np(q), to_np(k), to_np(v), to_np(dout), to_np(out), lse.cpu().numpy())
+    _check_all(f"backward sweep {i}", mode, inputs, (to_np(dq), to_np(dk), to_np(dv)),
+               (rq, rk, rv), block, window)
