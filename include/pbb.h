@@ -125,12 +125,13 @@ pbb_status_t pbb_ring_fill(const pbb_desc_t *desc, const int32_t *pos, const voi
 /*
  * Workspace bytes pbb_decode_step needs.  0 unless the launch is split: bf16 launches with at
  * most 64 (sequence, KV head) units whose block (or window) exceeds 256 keys spread each unit's
- * support over up to eight workgroups,
- * which leave partial softmax states (Eq.(lse), Appendix A.4) in the workspace for the last of
- * them to merge.  Its first 256-byte-aligned part holds one counter per unit: it must be
- * zero-filled before the first call, and every call leaves it zero again, so one allocation
- * serves every later call on one stream; calls that may run concurrently need separate
- * workspaces.  The size depends only on the descriptor.
+ * support over S = min(floor(256 / units), ceil(steps / 8), 8) workgroups (steps = 32-key steps
+ * of the longest support), which leave partial softmax states (Eq.(lse), Appendix A.4) in the
+ * workspace for the last of them to merge.  Its first 256 bytes hold one counter per unit: they
+ * must be zero-filled before the first call, and every call leaves them zero again, so one
+ * allocation serves every later call on one stream, for any descriptor it is large enough for;
+ * calls that may run concurrently need separate workspaces.  The size depends only on the
+ * descriptor.
  */
 pbb_status_t pbb_workspace_bytes(const pbb_desc_t *desc, size_t *bytes);
 

@@ -60,20 +60,18 @@ size_t ring_tensor_bytes(const pbb_desc_t* d) {
 // spread each unit's key steps over up to eight workgroups (at least eight 32-key steps each,
 // two per wave of a 4-wave workgroup), so that more of the chip streams the rings.  The merge
 // through the workspace costs a few serial device-coherent round trips (~2-3 us), which pays
-// off for small batches with long supports.
+// off for small batches with long supports.  The count is rounded down, so that a launch never
+// exceeds one workgroup per CU (one more round of workgroups would double its time when the
+// supports are equal, as in a full sliding window).
 int32_t decode_splits(const pbb_desc_t* d, bool swa) {
   if (d->dtype != PBB_DTYPE_BF16) return 1;
   const int64_t units = (int64_t)d->batch * d->n_kv_heads;
   if (units > kSplitMaxUnits) return 1;
   const int64_t max_steps = ((int64_t)(swa ? d->window : d->block) + 31) / 32;
-  int64_t s = std::min((kSplitUnits + units - 1) / units, (max_steps + 7) / 8);
+  int64_t s = std::min(kSplitUnits / units, (max_steps + 7) / 8);
   s = std::min<int64_t>(s, kSplitMaxWays);
   s = std::min<int64_t>(s, pbb::kMaxSplitStates / (d->n_q_heads / d->n_kv_heads));
   return (int32_t)std::max<int64_t>(1, s);
-}
-
-size_t counters_bytes(const pbb_desc_t* d) {
-  return ((size_t)d->batch * (size_t)d->n_kv_heads * 4 + 255) / 256 * 256;
 }
 
 size_t decode_workspace(const pbb_desc_t* d, bool swa) {
@@ -81,7 +79,7 @@ size_t decode_workspace(const pbb_desc_t* d, bool swa) {
   if (s <= 1) return 0;
   const size_t part = (size_t)d->batch * (size_t)d->n_kv_heads * (size_t)s *
                       (size_t)(d->n_q_heads / d->n_kv_heads) * (size_t)(d->head_dim + 2) * 4;
-  return counters_bytes(d) + (part + 255) / 256 * 256;
+  return pbb::kCounterBytes + (part + 255) / 256 * 256;
 }
 
 // `use_scratch`: the workspace, when the launch needs one, is the library's per-device scratch
@@ -119,7 +117,7 @@ pbb_status_t decode_common(const pbb_desc_t* desc, bool swa, const int32_t* pos,
   a.splits = need > 0 ? decode_splits(desc, swa) : 1;
   a.counters = need > 0 ? static_cast<uint32_t*>(workspace) : nullptr;
   a.ws_part = need > 0 ? reinterpret_cast<float*>(static_cast<unsigned char*>(workspace) +
-                                                  counters_bytes(desc))
+                                                  pbb::kCounterBytes)
                        : nullptr;
   a.pos = pos;
   a.pos_next = want_next ? pos_next : nullptr;

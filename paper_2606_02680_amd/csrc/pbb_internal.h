@@ -18,12 +18,18 @@ constexpr int32_t kMaxGroup = 16;         // query heads per KV head held by one
 constexpr int64_t kSplitMaxUnits = 64;    // bf16 decode launches with at most this many units split
 constexpr int64_t kSplitMaxWays = 8;      // workgroups per unit of a split launch, at most
 
-// Largest workspace a decode launch can need: the 256-byte counter block of at most
-// kSplitMaxUnits units, then their partial states (kSplitMaxWays splits x kMaxGroup heads x
-// (head_dim 128 + maximum + sum) floats each) -- 4,260,096 bytes.  The allocation-free entry
-// point keeps one buffer of this size per device.
+// Every decode workspace starts with a counter block of this size (one counter per unit of a
+// split launch, at most kSplitMaxUnits), whatever the descriptor, so that one workspace,
+// zero-filled once, serves split launches of every descriptor it is large enough for.
+constexpr size_t kCounterBytes = 256;
+static_assert(kCounterBytes >= (size_t)kSplitMaxUnits * 4, "counter block");
+
+// Largest workspace a decode launch can need: the counter block, then the partial states of
+// kSplitMaxUnits units (kSplitMaxWays splits x kMaxGroup heads x (head_dim 128 + maximum +
+// sum) floats each) -- 4,260,096 bytes.  The allocation-free entry point keeps one buffer of
+// this size per device.
 constexpr size_t kNoAllocScratchBytes =
-    256 + (size_t)kSplitMaxUnits * kSplitMaxWays * kMaxGroup * (128 + 2) * 4;
+    kCounterBytes + (size_t)kSplitMaxUnits * kSplitMaxWays * kMaxGroup * (128 + 2) * 4;
 
 // Everything a decode kernel needs, validated on the host before launch.
 struct DecodeArgs {

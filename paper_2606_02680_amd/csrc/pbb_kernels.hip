@@ -485,8 +485,9 @@ void decode_f32_mfma_kernel(DecodeArgs a) {
 // the step sits at a fixed per-lane offset from the range's first row; only steps that cross a
 // range boundary, the current token or the end compute slots per lane.  The current token's row
 // is not read from the ring: its K and V rows are loaded into registers at launch, and the wave
-// that owns its step writes them into its LDS tiles (the DMA of that row reads slot 0, which is
-// then overwritten).  No loaded value other than these lands in a register, so the only memory
+// that owns its step writes them into its LDS tiles (the DMA of that row, and of the padding
+// after it, reads the support's first ring slot; the row is then overwritten).  No loaded value
+// other than these lands in a register, so the only memory
 // waits are the explicit vmcnt(OPS) at the top of a step: loads retire in issue order and
 // exactly OPS loads (the next step's) are issued after the current step's.  Steps past the
 // end are still issued (reading slot 0) to keep that count fixed.  Padded heads (h >= G)
@@ -573,6 +574,7 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
   }
   const Ranges R = ranges_for(a, t);
   const int n_total = R.n_ring + 1;
+  const int pad_slot = R.n_ring > 0 ? ring_slot(R, 0) : 0;   // a slot the support reads
   uint16_t* kring = (uint16_t*)a.k_ring + (size_t)bg * a.slots * D;
   uint16_t* vring = (uint16_t*)a.v_ring + (size_t)bg * a.slots * D;
   const uint16_t* knew = (const uint16_t*)a.k_new + (size_t)bg * D;
@@ -663,14 +665,17 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
 #pragma unroll
       for (int x = 0; x < NG; ++x) dma(vring_b + sh, x, rowoff[x], 1);
     } else {
-      // Per-lane slots: range boundary, current token (read from slot 0, replaced in LDS) or
-      // rows past this workgroup's steps (slot 0, never used).
+      // Per-lane slots: range boundary, the current token and the padding after it (read from
+      // the support's first ring slot, pad_slot: real data, whose weights are then 0; the
+      // current token's row is replaced in LDS), or rows past this workgroup's steps (slot 0,
+      // never used).
       uint32_t off[NG];
 #pragma unroll
       for (int x = 0; x < NG; ++x) {
         const int row = x * RPI + lane / PPR;
         const int i = k0 + row;
-        const int slot = (k0 >= k_lim || i >= R.n_ring) ? 0 : (i < R.len0 ? R.base0 + i : i - R.len0);
+        const int slot = k0 >= k_lim ? 0
+                         : (i >= R.n_ring ? pad_slot : (i < R.len0 ? R.base0 + i : i - R.len0));
         off[x] = (uint32_t)(slot * ROWB + (((lane % PPR) ^ swz(row)) << 4));
       }
 #pragma unroll
@@ -704,17 +709,18 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
     // This step's tiles have landed once at most the next step's OPS loads are outstanding.
     __builtin_amdgcn_s_waitcnt(0x0F70 | (OPS & 15) | ((OPS >> 4) << 14));
     if (step == cur_step) {
-      // The current token's row arrived from slot 0: overwrite it with k_new / v_new (the
-      // turned key in rotary mode).  The V rows after it (this step's padding, also DMA'd
-      // from slot 0) are zeroed: their weights are 0, but slot 0 may hold bits that were
-      // never written (0 * NaN would reach the output).  Padded K rows need nothing: their
-      // scores are replaced by -inf below.
+      // The current token's row arrived from pad_slot: overwrite it with k_new / v_new (the
+      // turned key in rotary mode).  The rows after it (this step's padding) get weight 0; they
+      // hold the support's first ring row, so 0 * V stays 0.  A support with no ring key
+      // (t = 0) has no such row: its padding came from slot 0, which may hold bits that were
+      // never written (0 * NaN would reach the output), so its V rows are zeroed.  Padded K
+      // rows need nothing: their scores are replaced by -inf below.
       const int rc = R.n_ring & 31;
       unsigned char* tile = wbuf + BO;
-      {
+      if (R.n_ring == 0) {
         const u32x4 zero = {0u, 0u, 0u, 0u};
-        for (int e = lane; e < (31 - rc) * PPR; e += 64)
-          *(u32x4*)(tile + TILE + (rc + 1 + e / PPR) * ROWB + (e % PPR) * 16) = zero;
+        for (int e = lane; e < 31 * PPR; e += 64)
+          *(u32x4*)(tile + TILE + (1 + e / PPR) * ROWB + (e % PPR) * 16) = zero;
       }
       if constexpr (ROPE) {
         if (lane < PPR / 2) {
@@ -1014,10 +1020,10 @@ hipError_t noalloc_scratch(void** ptr, hipStream_t stream) {
     e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
     if (e != hipSuccess) return e;
     if (p == nullptr) return hipErrorInvalidSymbol;
-    // The unit counters must start at zero (every split launch leaves them zero again); the
-    // block is cleared by a fill kernel, which a graph capture may record.
+    // The counter block must start at zero (every launch leaves it zero again); it is cleared
+    // by a fill kernel, which a graph capture may record.
     hipLaunchKernelGGL(scratch_clear_kernel, dim3(1), dim3(64), 0, stream, (uint4*)p,
-                       (size_t)(256 / 16));
+                       pbb::kCounterBytes / 16);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     addr[dev] = p;

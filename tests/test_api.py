@@ -253,12 +253,12 @@ def test_split_decode_workspace():
     """bf16 launches with at most 64 (sequence, KV head) units split each unit over up to eight
     workgroups and need a workspace: counters (256-byte aligned) plus partial states."""
     one = B.make_desc(1, 32, 8, 128, block=2048, dtype=torch.bfloat16)
-    # 8 units -> min(ceil(256 / 8), ceil(64 / 8), 8) = 8 workgroups per unit
+    # 8 units -> min(floor(256 / 8), ceil(64 / 8), 8) = 8 workgroups per unit
     assert P.workspace_bytes(one) == 256 + 8 * 8 * 4 * (128 + 2) * 4
     swa = B.make_desc(2, 8, 2, 128, window=4096, slots=4096, dtype=torch.bfloat16)
     assert P.swa_workspace_bytes(swa) == 256 + 4 * min(64, 16, 8) * 4 * 130 * 4
     mid = B.make_desc(5, 32, 8, 128, block=2048, dtype=torch.bfloat16)    # 40 units
-    assert P.workspace_bytes(mid) == 256 + 40 * 7 * 4 * 130 * 4           # ceil(256 / 40) = 7
+    assert P.workspace_bytes(mid) == 256 + 40 * 6 * 4 * 130 * 4           # floor(256 / 40) = 6
     many = B.make_desc(9, 32, 8, 128, block=2048, dtype=torch.bfloat16)   # 72 units
     assert P.workspace_bytes(many) == 0
     short = B.make_desc(1, 32, 8, 128, block=256, dtype=torch.bfloat16)   # 8 steps at most
@@ -276,7 +276,7 @@ def test_split_decode_workspace():
 
 def test_split_rule_over_random_descriptors():
     """The documented split rule, restated: bf16 launches with at most 64 (sequence, KV head)
-    units split each unit over S = min(ceil(256 / units), ceil(steps / 8), 8) workgroups
+    units split each unit over S = min(floor(256 / units), ceil(steps / 8), 8) workgroups
     (steps = ceil(B / 32) or ceil(W / 32)); S > 1 needs 256-byte-aligned counters plus
     units * S * G * (d + 2) floats."""
     import numpy as np
@@ -297,7 +297,7 @@ def test_split_rule_over_random_descriptors():
             got = P.workspace_bytes(desc)
         units = batch * hkv
         steps = -(-span // 32)
-        S = min(-(-256 // units), -(-steps // 8), 8) if units <= 64 else 1
+        S = min(256 // units, -(-steps // 8), 8) if units <= 64 else 1
         if dt != torch.bfloat16 or S <= 1:
             assert got == 0, (batch, hkv, G, d, swa, span, dt)
             continue

@@ -292,6 +292,8 @@ def test_snapshot_restore_continues_bitwise(cuda):
     ("swa", 2, 128, 8, 2, 0, 4096, 4096, 300000, 4),    # 8 splits
     ("pbb", 8, 128, 32, 8, 2048, 0, 2048, 300000, 3),   # 64 units: 4 splits
     ("swa", 10, 64, 16, 4, 0, 1000, 1024, 90000, 3),    # 40 units: 4 splits
+    ("pbb", 5, 128, 32, 8, 2048, 0, 2048, 300000, 3),   # 40 units: floor(256 / 40) = 6 splits
+    ("swa", 6, 128, 32, 8, 0, 4096, 4096, 300000, 3),   # 48 units, full windows: 5 splits
 ])
 def test_split_workgroups_small_batch(cuda, mode, batch, d, hq, hkv, block, window, slots,
                                       pos_hi, steps):
@@ -317,6 +319,29 @@ def test_split_workgroups_small_batch(cuda, mode, batch, d, hq, hkv, block, wind
     # the launches left every unit counter at zero
     units = batch * hkv
     assert not run.ws[: 4 * units].any().item()
+
+
+def test_one_workspace_for_split_launches_of_two_descriptors(cuda):
+    """One caller workspace, zero-filled once, serves split launches of two descriptors in turn
+    (64 units in 4 splits, 16 units in 8): both keep their counters in the first 256 bytes, so
+    the partial states of one never land on the other's counters."""
+    base = W.get_config("c3")
+    runs = []
+    for batch in (8, 2):
+        cfg = base.with_(batch=batch, name=f"shared-ws-{batch}")
+        runs.append(Run(cfg, W.initial_positions(cfg), 4, cuda))
+    assert all(r.ws is not None for r in runs)
+    ws = torch.zeros(max(r.ws.numel() for r in runs), dtype=torch.uint8, device=cuda)
+    for r in runs:
+        r.ws = ws
+    hists = [r.history(np.arange(r.cfg.batch), 3) for r in runs]
+    for i in range(4):
+        for r, hist in zip(runs, hists):
+            q, out = r.step()
+            rows = np.arange(r.cfg.batch)
+            compare(r.cfg, to_np(out), r.oracle_out(rows, i, q, hist=hist),
+                    what=f"{r.cfg.name} step {i}")
+            assert not ws[:256].any().item(), f"{r.cfg.name} step {i}: counters not zero"
 
 
 @pytest.mark.parametrize("mode,dtype,d,hq,hkv,block,window,slots,rope", [
