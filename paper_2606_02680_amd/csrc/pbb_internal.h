@@ -17,6 +17,11 @@ constexpr int kMaxSplitStates = 2048;
 constexpr int32_t kMaxGroup = 16;         // query heads per KV head held by one MFMA tile
 constexpr int64_t kSplitMaxUnits = 64;    // bf16 decode launches with at most this many units split
 constexpr int64_t kSplitMaxWays = 8;      // workgroups per unit of a split launch, at most
+// bf16 decode launches with at most this many units over rings of at most this many slots
+// prefetch the whole ring (one 32-slot chunk per wave of a 4-wave workgroup) at entry.
+constexpr int32_t kWholeRingMaxUnits = 256;
+constexpr int32_t kWholeRingMaxSlots = 128;
+constexpr int kWholeRingWaves = 4;        // waves per workgroup of those launches
 
 // Every decode workspace starts with a counter block of this size (one counter per unit of a
 // split launch, at most kSplitMaxUnits), whatever the descriptor, so that one workspace,

