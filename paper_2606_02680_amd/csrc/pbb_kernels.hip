@@ -548,14 +548,16 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
   // Step buffers per wave: two (a two-deep pipeline), or in whole-ring mode one per ring chunk
   // of the wave (chunks w, w + NW, ... of at most kWholeRingMaxSlots / 32).
   constexpr int CPW = WR ? (kWholeRingMaxSlots / 32 + NW - 1) / NW : 2;
-  constexpr int NBUF = CPW > 2 ? CPW : 2;
+  constexpr int NBUF = WR ? CPW : 2;
   constexpr int STAGE_BYTES = NW * NBUF * BUF;
   constexpr int MERGE_BYTES = NW * 16 * (D + 2) * 4;
   // Split launches merge up to kMaxSplitStates (splits x heads) states through LDS after the
-  // wave merge area and the arrival flag.
+  // wave merge area and the arrival flag.  Whole-ring launches keep the merge area after the
+  // step buffers (no barrier before the partial states are written).
   constexpr int SPLIT_BYTES = SPLIT ? (2 * kMaxSplitStates + 16) * 4 : 0;
-  constexpr int SMEM = STAGE_BYTES > MERGE_BYTES + 16 + SPLIT_BYTES ? STAGE_BYTES
-                                                                    : MERGE_BYTES + 16 + SPLIT_BYTES;
+  constexpr int SMEM = WR ? STAGE_BYTES + MERGE_BYTES + 16
+                          : (STAGE_BYTES > MERGE_BYTES + 16 + SPLIT_BYTES ? STAGE_BYTES
+                                                                          : MERGE_BYTES + 16 + SPLIT_BYTES);
   __shared__ __align__(16) unsigned char smem[SMEM];
 
   const int S = SPLIT ? a.splits : 1;
@@ -950,6 +952,27 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
     const u32x4 zero = {0u, 0u, 0u, 0u};
     qB[kk] = __builtin_bit_cast(bf16x8, c16 < G ? qload[kk] : zero);
   }
+  auto append_token = [&]() {
+    // Fused append of the current token (by the unit's first workgroup).  Slot t mod slots
+    // holds a position outside the support of t (and of every later step).
+    if (wave == 0 && sp == 0) {
+      if constexpr (ROPE) {
+        if (lane < PPR / 2) {
+          uint16_t* dst = kring + (size_t)R.append_slot * D;
+          *(u32x4*)(dst + lane * 8) = krot_lo;
+          *(u32x4*)(dst + D / 2 + lane * 8) = krot_hi;
+        }
+        if (rowlane && lane >= PPR)
+          *(u32x4*)(vring + (size_t)R.append_slot * D + (lane % PPR) * 8) = cur_row;
+      } else if (rowlane) {
+        *(u32x4*)((lane < PPR ? kring : vring) + (size_t)R.append_slot * D + (lane % PPR) * 8) =
+            cur_row;
+      }
+    }
+  };
+  // Whole-ring launches append right away: every ring load of the launch has completed, so the
+  // store overlaps the computation instead of ending the launch.
+  if constexpr (WR) append_token();
   if constexpr (WR) {
     // each wave computes its chunks that hold some slot of the support, one copy of the step
     // code in a loop
@@ -982,8 +1005,8 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
   // l per head: sum the four quarters' partial sums.
   lsum = sum_xor16_32(lsum);
 
-  __syncthreads();  // every wave is done with its tiles: reuse LDS for the merge
-  float* sm_acc = (float*)smem;              // [NW][16 heads][D]
+  if constexpr (!WR) __syncthreads();  // every wave is done with its tiles: reuse LDS for the merge
+  float* sm_acc = (float*)(smem + (WR ? STAGE_BYTES : 0));   // [NW][16 heads][D]
   float* sm_m = sm_acc + NW * 16 * D;         // [NW][16]
   float* sm_l = sm_m + NW * 16;               // [NW][16]
   if (c16 < G) {
@@ -1100,23 +1123,9 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
     }
   }
 
-  // Fused append of the current token (by the unit's first workgroup).  Slot t mod slots holds
-  // a position outside the support of t (and of every later step), so no read of this launch
-  // can observe the write.
-  if (wave == 0 && sp == 0) {
-    if constexpr (ROPE) {
-      if (lane < PPR / 2) {
-        uint16_t* dst = kring + (size_t)R.append_slot * D;
-        *(u32x4*)(dst + lane * 8) = krot_lo;
-        *(u32x4*)(dst + D / 2 + lane * 8) = krot_hi;
-      }
-      if (rowlane && lane >= PPR)
-        *(u32x4*)(vring + (size_t)R.append_slot * D + (lane % PPR) * 8) = cur_row;
-    } else if (rowlane) {
-      *(u32x4*)((lane < PPR ? kring : vring) + (size_t)R.append_slot * D + (lane % PPR) * 8) =
-          cur_row;
-    }
-  }
+  // Stepped launches append at the end: no read of this launch can observe the write (the slot
+  // holds a position outside the support).
+  if constexpr (!WR) append_token();
 }
 
 }  // namespace
