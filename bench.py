@@ -22,6 +22,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -49,12 +50,30 @@ def step_bytes(t, cfg):
     return int(per_seq.sum())
 
 
-def _kernel_hash():
-    """Hash of the sources that define the decode kernels (counter summaries are tied to it)."""
+_DECODE_SOURCES = ("pbb_kernels.hip", "pbb_device.h", "pbb_internal.h", "pbb_api.cpp")
+
+
+def _code_only(text):
+    """Source text without // comments, blank lines and runs of whitespace."""
+    out = []
+    for ln in text.splitlines():
+        ln = re.sub(r"\s+", " ", re.sub(r"//.*$", "", ln)).strip()
+        if ln:
+            out.append(ln)
+    return "\n".join(out)
+
+
+def _kernel_hash(read=None):
+    """Hash of the code that defines and selects the decode kernels (counter summaries are tied
+    to it; comments do not count).  ``read(name)`` returns a source's text (default: the
+    working tree)."""
+    if read is None:
+        def read(name):
+            with open(os.path.join(ROOT, "paper_2606_02680_amd", "csrc", name)) as fh:
+                return fh.read()
     h = hashlib.sha256()
-    for f in ("pbb_kernels.hip", "pbb_device.h"):
-        with open(os.path.join(ROOT, "paper_2606_02680_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+    for f in _DECODE_SOURCES:
+        h.update(_code_only(read(f)).encode())
     return h.hexdigest()[:16]
 
 

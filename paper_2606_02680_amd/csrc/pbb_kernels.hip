@@ -487,12 +487,22 @@ void decode_f32_mfma_kernel(DecodeArgs a) {
 // is not read from the ring: its K and V rows are loaded into registers at launch, and the wave
 // that owns its step writes them into its LDS tiles (the DMA of that row, and of the padding
 // after it, reads the support's first ring slot; the row is then overwritten).  No loaded value
-// other than these lands in a register, so the only memory
-// waits are the explicit vmcnt(OPS) at the top of a step: loads retire in issue order and
-// exactly OPS loads (the next step's) are issued after the current step's.  Steps past the
-// end are still issued (reading slot 0) to keep that count fixed.  Padded heads (h >= G)
-// compute on zero queries and are never stored.  Wave results are merged through LDS with
-// Eq.(lse) (Appendix A.4) and written as bf16 (RNE).
+// other than these lands in a register, so the only memory waits are the explicit vmcnt(OPS)
+// at the top of a step: loads retire in issue order and exactly OPS loads (the next step's) are
+// issued after the current step's.  Steps past the end are still issued (reading slot 0) to
+// keep that count fixed.  Padded heads (h >= G) compute on zero queries and are never stored.
+// Wave results are merged through LDS with Eq.(lse) (Appendix A.4), four channels per thread,
+// and written as bf16 (RNE).
+//
+// Launch kinds.  The position is read through the scalar cache (no launch writes pos) after the
+// queries and the current token's rows have been requested, so waiting for it does not wait for
+// vector loads.  Whole-ring launches (WR: few units over rings of at most kWholeRingMaxSlots,
+// where a step is latency-bound) issue the ring's 32-slot chunks, one per wave, before the
+// position is known, and mask each chunk to the support afterwards: a 32-bit slot mask built
+// from the two slot ranges sets the scores outside the support to -inf and zeroes their value
+// operands in registers (slots never written may hold NaN bits); they append the current token
+// as soon as the ring's loads have landed.  Split launches (SPLIT) spread a unit's steps over
+// several workgroups that merge through the workspace (below).
 //
 // Tile layout.  One 16-byte DMA of the wave writes 1 KiB: lane l lands at byte 16 l, i.e. RPI
 // whole rows.  Piece p of row r sits at piece slot p ^ swz(r), with swz(r) = 2 (r mod 8) for
