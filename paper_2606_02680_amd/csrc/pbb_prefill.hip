@@ -33,7 +33,7 @@ namespace {
 constexpr int kPrefillWaves128 = 4;
 constexpr int kPrefillWaves64 = 4;
 constexpr int kPrefillStages128 = 3;
-constexpr int kPrefillStages64 = 3;
+constexpr int kPrefillStages64 = 5;  // a tile at d = 64 walks few key steps: all in flight early
 constexpr int kPrefillColGroups128 = 2;
 constexpr int kPrefillColGroups64 = 2;
 
