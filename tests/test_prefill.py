@@ -211,13 +211,16 @@ def test_prefill_largest_ring_sampled(cuda, mode, hq, hkv, block, window):
                                   block=block, window=window)[0] for i, tt in enumerate(t)])
     got = to_np(out[0, torch.as_tensor(t, device=cuda)])
     compare(cfg, got, ref, what=f"{cfg.name} sampled positions")
-    # log-partitions: the dense masked softmax of each sampled position, in fp64
+    # log-partitions in fp64 over each sampled position's support as the oracle's two-case
+    # membership test (Eq.(pbb), Prop. 2) gives it
     scale = 1.0 / np.sqrt(64.0)
     G = hq // hkv
     for i, tt in enumerate(t):
-        lo = max(0, h * (tt // h - 1)) if mode == "pbb" else max(0, tt - window + 1)
+        tt = int(tt)
+        sup = np.array(oracle.pbb_support(tt, block) if mode == "pbb"
+                       else oracle.swa_support(tt, window), dtype=np.int64)
         for hd in range(hq):
-            z = kh[0, hd // G, lo:tt + 1].astype(np.float64) @ qs[i, hd].astype(np.float64) * scale
+            z = kh[0, hd // G, sup].astype(np.float64) @ qs[i, hd].astype(np.float64) * scale
             ref_lse = z.max() + np.log(np.exp(z - z.max()).sum())
             assert abs(float(lse[0, hd, tt]) - ref_lse) <= 2e-3, (tt, hd)
     # ring: slot s mod slots holds the last prompt position s
