@@ -164,13 +164,18 @@ class Workload:
 
         Two passes over the same steps from the same state (rings and positions restored from a
         snapshot taken after the warmup):
-          * eager: back-to-back launches on one stream with HIP events around each launch on
-            that stream -> ``kernel_s``, the mean kernel duration (the roofline's figure);
-          * graph (``graph=True``): the same launches captured as one HIP graph, replayed once
+          * graph (``graph=True``): the launches captured as one HIP graph, replayed once
             untimed and once timed -> ``wall_s``, the wall clock of the whole replay between
             two synchronisations (the throughput figure), and ``graph_event_s``, HIP events
-            around it.
-        Without ``graph``, ``wall_s`` is the eager loop's wall clock.  ``bytes``: algorithmic
+            on the launch stream around it;
+          * eager: back-to-back launches on one stream with HIP events around each launch on
+            that stream -> ``eager_kernel_s``, the mean of those per-launch intervals.
+        ``kernel_s`` (the roofline's duration) is ``graph_event_s`` per step with ``graph``: the
+        mean launch duration over the timed region, the short gaps between graph nodes
+        included; a pair of events around every eager launch adds a few microseconds of
+        launch overhead to each interval (rocprof's kernel durations agree with the graph
+        figure, and sit ~2% below the per-launch one).  Without ``graph``, ``kernel_s`` is
+        ``eager_kernel_s`` and ``wall_s`` the eager loop's wall clock.  ``bytes``: algorithmic
         bytes of the timed steps (their actual positions)."""
         import torch
         for i in range(warmup):
@@ -227,8 +232,11 @@ class Workload:
         res["eager_wall_s"] = time.perf_counter() - w0
         if steps % 2:
             self.pos.copy_(self.pos_next)   # self.pos holds the next position, as after step()
-        res["kernel_s"] = sum(s.elapsed_time(e) for s, e in zip(starts, ends)) / 1e3 / steps
-        if not graph:
+        res["eager_kernel_s"] = sum(s.elapsed_time(e) for s, e in zip(starts, ends)) / 1e3 / steps
+        if graph:
+            res["kernel_s"] = res["graph_event_s"] / steps
+        else:
+            res["kernel_s"] = res["eager_kernel_s"]
             res["wall_s"] = res["eager_wall_s"]
         del snap
         return res
@@ -869,13 +877,16 @@ def main(argv=None):
                    "head_dim": cfg.d, "block": cfg.block, "slots": cfg.slots,
                    "window": cfg.window, "parallelism": "single GPU"},
         "timing": ("steps captured as one HIP graph (one launch per step, positions advanced on "
-                   "the device), wall clock of the replay; kernel time from a second, eager pass "
-                   "over the same steps with HIP events around each launch"
+                   "the device): value from the wall clock of the replay, kernel time (roofline) "
+                   "from HIP events on the launch stream around the replay, per step; a second, "
+                   "eager pass over the same steps with HIP events around each launch gives "
+                   "eager_kernel_us"
                    if not args.no_graph else
                    "eager back-to-back launches with HIP events around each launch"),
         "hbm_gbps_step": total_bytes / elapsed / 1e9,
         "bytes_per_token": total_bytes / tokens,
         "kernel_us": kern_s * 1e6,
+        "eager_kernel_us": tm["eager_kernel_s"] * 1e6,
         "eager_ms_per_step": tm["eager_wall_s"] / args.steps * 1e3,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS,
