@@ -273,15 +273,18 @@ __global__ __launch_bounds__(256) void decode_f32_kernel(DecodeArgs a) {
 // into registers as matrix-core operands, the next tile's loads in flight while the current tile
 // computes.  Lane l works in quarter j = l / 16 on row l % 16 of each 16 x 16 tile:
 //   scores  S^T[16 keys][16 heads] = K Q^T in D/4 MFMAs; MFMA m contracts channel
-//           (D/4) j + m in quarter j, so lane (key l%16, j) reads D/4 consecutive channels of
-//           its key row, and the B operand holds the queries (scaled by scale * log2 e, zero for
-//           heads past G).  The result gives lane (head l%16, j) keys 4j..4j+3 of the tile.
+//           16 (m / 4) + 4 j + m mod 4 in quarter j, so lane (key l%16, j) reads channels
+//           16 x + 4 j .. +3 of its key row (x < D/16): each 16-byte load of the wave then
+//           takes 64 contiguous bytes of each of 16 rows.  The B operand holds the queries
+//           under the same map (scaled by scale * log2 e, zero for heads past G).  The result
+//           gives lane (head l%16, j) keys 4j..4j+3 of the tile.
 //   softmax column maxima across the quarters by permlane swaps; the reference moves only when
 //           a column's maximum exceeds it by more than 8 (log2 units), decided wave-uniformly.
-//   values  O^T += V^T P^T in D/4 MFMAs: row r of output tile nb is channel (D/16) r + nb and
-//           MFMA (nb, m) contracts key 4j + m in quarter j, so the B operand is the lane's own
-//           weight of key 4j + m and lane (r, j) reads D/16 consecutive channels of each of
-//           its four key rows.
+//   values  O^T += V^T P^T in D/4 MFMAs: row r of output tile nb is channel
+//           64 (nb / 4) + 4 r + nb mod 4 and MFMA (nb, m) contracts key 4j + m in quarter j, so
+//           the B operand is the lane's own weight of key 4j + m and lane (r, j) reads channels
+//           64 y + 4 r .. +3 (y < D/64) of each of its four key rows: each 16-byte load of the
+//           wave takes 256 contiguous bytes of each of 4 rows.
 // Waves merge through LDS with Eq.(lse) (Appendix A.4); the append of the current token is
 // done last (its slot is never read in the launch).
 // Groups from this size on take the matrix-core fp32 kernel (a single query head per KV head
@@ -329,9 +332,10 @@ void decode_f32_mfma_kernel(DecodeArgs a) {
   float qf[KM];
   {
     const float* qrow = (const float*)a.q + ((size_t)b * a.hq + (size_t)g * G +
-                                             (size_t)(c16 < G ? c16 : 0)) * D + KM * j4;
+                                             (size_t)(c16 < G ? c16 : 0)) * D + 4 * j4;
 #pragma unroll
-    for (int m = 0; m < KM; ++m) qf[m] = c16 < G ? qrow[m] * a.scale_log2 : 0.0f;
+    for (int m = 0; m < KM; ++m)
+      qf[m] = c16 < G ? qrow[16 * (m >> 2) + (m & 3)] * a.scale_log2 : 0.0f;
   }
   // Row of key i of the unit: a ring slot, the current token, or (past the end) the current
   // token again, masked out of the softmax.
@@ -343,14 +347,14 @@ void decode_f32_mfma_kernel(DecodeArgs a) {
   };
   auto load = [&](int tile, f4 (&kb)[KQ], f4 (&vb)[4][VQ]) __attribute__((always_inline)) {
     const int i0 = tile * 16;
-    const float* kp = krow(i0 + c16) + KM * j4;
+    const float* kp = krow(i0 + c16) + 4 * j4;
 #pragma unroll
-    for (int q = 0; q < KQ; ++q) kb[q] = *(const f4*)(kp + 4 * q);
+    for (int q = 0; q < KQ; ++q) kb[q] = *(const f4*)(kp + 16 * q);
 #pragma unroll
     for (int m = 0; m < 4; ++m) {
-      const float* vp = vrow(i0 + 4 * j4 + m) + E * c16;
+      const float* vp = vrow(i0 + 4 * j4 + m) + 4 * c16;
 #pragma unroll
-      for (int q = 0; q < VQ; ++q) vb[m][q] = *(const f4*)(vp + 4 * q);
+      for (int q = 0; q < VQ; ++q) vb[m][q] = *(const f4*)(vp + 64 * q);
     }
   };
 
@@ -430,7 +434,8 @@ void decode_f32_mfma_kernel(DecodeArgs a) {
 #pragma unroll
     for (int nb = 0; nb < E; ++nb)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) sm_acc[wave][c16][E * (4 * j4 + i) + nb] = acc[nb][i];
+      for (int i = 0; i < 4; ++i)
+        sm_acc[wave][c16][64 * (nb >> 2) + 4 * (4 * j4 + i) + (nb & 3)] = acc[nb][i];
     if (j4 == 0) {
       sm_m[wave][c16] = mref;
       sm_l[wave][c16] = lsum;

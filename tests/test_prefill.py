@@ -227,3 +227,53 @@ def test_prefill_largest_ring_sampled(cuda, mode, hq, hkv, block, window):
     kb = bits(kr[0])
     for s in (n - 1, n - 2, n - B if n - B >= 0 else 0, n - 40000):
         assert np.array_equal(kb[:, s % desc.slots], bits(k[0, s]).reshape(hkv, -1)), s
+
+
+@pytest.mark.parametrize("mode,block,window,slots", [
+    ("pbb", 128, 0, 128),
+    ("swa", 0, 128, 256),
+])
+def test_rotary_prompt_prefill_then_rotary_decode(cuda, mode, block, window, slots):
+    """The paper's inference path at its head shape (Hq 12, Hkv 2, head_dim 64, B 128; RoPE
+    base 10^6, App. C; cached prefill then sequential decoding, App. F.7): the prompt's q and k
+    are turned by position (the oracle's exact rotation, rounded to bf16) and go through
+    prefill, whose ring -- rotated keys -- then feeds decode steps that turn q and the new key
+    themselves.  Prefill outputs match the oracle prefill of the turned prompt; every decode
+    step matches the oracle, which turns the raw history keys exactly at their positions."""
+    base, n, steps = 1e6, 700, 40
+    cfg = _cfg(mode, 1, n + steps, 12, 2, 64, block, window, slots).with_(rope_base=base)
+    qa, ka, va = W.prompt(cfg.with_(rope_base=0.0), n + steps, device=cuda)  # raw q, k, v
+    idx = np.arange(n)[None, :, None]                                      # position of each row
+    qr = torch.from_numpy(oracle.rope_rows(to_np(qa[:, :n]), idx, base)).to(cuda, torch.bfloat16)
+    kr_ = torch.from_numpy(oracle.rope_rows(to_np(ka[:, :n]), idx, base)).to(cuda, torch.bfloat16)
+    vp = va[:, :n].contiguous()
+    plain = (P.make_desc(1, 12, 2, 64, window=window, slots=slots, dtype=torch.bfloat16)
+             if mode == "swa" else P.make_desc(1, 12, 2, 64, block=block, dtype=torch.bfloat16))
+    rot = (P.make_desc(1, 12, 2, 64, window=window, slots=slots, dtype=torch.bfloat16,
+                       rope_base=base)
+           if mode == "swa" else P.make_desc(1, 12, 2, 64, block=block, dtype=torch.bfloat16,
+                                             rope_base=base))
+    kring, vring = P.alloc_rings(plain, cuda)
+    P.ring_init(plain, kring, vring)
+    out = torch.empty_like(qr)
+    lse = torch.empty((1, 12, n), dtype=torch.float32, device=cuda)
+    print(f"[prefill] rotary prompt then rotary decode, {mode}", flush=True)
+    (P.swa_prefill if mode == "swa" else P.pbb_prefill)(plain, qr, kr_, vp, out, lse, kring, vring)
+    torch.cuda.synchronize()
+    m = oracle.SWA if mode == "swa" else oracle.PBB
+    ref, ref_lse = oracle.prefill(m, to_np(qr), to_np(kr_), to_np(vp), block=block, window=window)
+    compare(cfg.with_(rope_base=0.0), to_np(out), ref, what=f"{mode} rotary-prompt prefill")
+    assert np.abs(lse.cpu().numpy().astype(np.float64) - ref_lse).max() <= 2e-3
+    kh = to_np(ka.permute(0, 2, 1, 3).contiguous())     # raw history [1][Hkv][n+steps][d]
+    vh = to_np(va.permute(0, 2, 1, 3).contiguous())
+    pos = torch.full((1,), n, dtype=torch.int32, device=cuda)
+    step = P.swa_decode_step if mode == "swa" else P.pbb_decode_step
+    for i in range(steps):
+        t = n + i
+        qd = qa[:, t].contiguous()
+        o = torch.empty_like(qd)
+        step(rot, pos, qd, ka[:, t].contiguous(), va[:, t].contiguous(), kring, vring, o)
+        pos += 1
+        ref = oracle.decode(m, np.array([t]), to_np(qd), kh[:, :, :t + 1], vh[:, :, :t + 1],
+                            np.zeros(1, np.int64), block=block, window=window, rope_base=base)
+        compare(cfg, to_np(o), ref, what=f"{mode} rotary decode after rotary prefill, t={t}")
