@@ -18,7 +18,7 @@ import oracle
 import paper_2606_02680_amd as P
 import workloads as W
 from tests.grad_bounds import U_BF16, grad_bounds
-from tests.harness import to_np
+from tests.harness import record_stats, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -54,6 +54,10 @@ def _grad_ok(name, got, ref, bound, heads_axis=2):
     cos = (gb * rb).sum(1) / np.maximum(np.linalg.norm(gb, axis=1) * rnb, 1e-30)
     assert rel.max() <= 2e-2, f"{name}: relative L2 {rel.max():.3e}"
     assert cos.min() >= 0.9998, f"{name}: cosine {cos.min():.6f}"
+    record_stats(name, {"max_abs": float(err.max()), "max_ref": rmax,
+                        "worst_error_over_derived_bound": worst, "rel_l2_total": float(tot),
+                        "cos_total": cos_t, "rel_l2_max_slice": float(rel.max()),
+                        "cos_min_slice": float(cos.min())})
     return worst
 
 

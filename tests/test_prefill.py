@@ -18,7 +18,7 @@ import torch
 import oracle
 import paper_2606_02680_amd as P
 import workloads as W
-from tests.harness import bits, compare, to_np
+from tests.harness import bits, compare, error_stats, record_stats, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -62,6 +62,8 @@ def _check(cfg, n, device, rings=True):
     got_lse = lse.cpu().numpy().astype(np.float64)
     assert np.isfinite(got_lse).all()
     assert np.abs(got_lse - ref_lse).max() <= 2e-3, np.abs(got_lse - ref_lse).max()
+    record_stats(cfg.name, {**error_stats(to_np(out), ref),
+                            "lse_max_abs": float(np.abs(got_lse - ref_lse).max())})
     if rings:
         kh = k.permute(0, 2, 1, 3).contiguous().cpu()
         vh = v.permute(0, 2, 1, 3).contiguous().cpu()
@@ -183,6 +185,9 @@ def test_prefill_bench_shapes(cuda, name, shape):
             compare(cfg, got, ref[:, first:], what=f"{name} seq {b} group {g} [{a0 + first}, {a1})")
             gl = lse[b:b + 1, hs, a0 + first:a1].cpu().numpy().astype(np.float64)
             assert np.abs(gl - ref_lse[:, :, first:]).max() <= 2e-3
+            record_stats(f"{name} seq {b} group {g} [{a0 + first}, {a1})",
+                         {**error_stats(got, ref[:, first:]),
+                          "lse_max_abs": float(np.abs(gl - ref_lse[:, :, first:]).max())})
 
 
 @pytest.mark.parametrize("mode,hq,hkv,block,window", [
