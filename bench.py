@@ -525,7 +525,7 @@ def _error_stats(got, ref):
                                                           1e-30)).min())}
 
 
-def cpu_baseline(cfg, t0, device, budget_s=10.0, max_steps=48, threads=None,
+def cpu_baseline(cfg, t0, device, budget_s=10.0, max_steps=64, threads=None,
                  single_thread=True):
     """The fp64 CPU oracle timed on FULL-BATCH decode steps of the workload: steps 0, 1, 2, ..
     (every sequence, every query head) with all host threads until ``budget_s`` seconds have
