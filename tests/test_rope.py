@@ -17,7 +17,7 @@ import torch
 
 import paper_2606_02680_amd as P
 import workloads as W
-from tests.harness import Run, bits, compare, to_np
+from tests.harness import Run, bits, compare, error_stats, merge_stats, record_stats, to_np
 
 pytestmark = pytest.mark.gpu
 
@@ -131,3 +131,38 @@ def test_rope_split_launch(cuda):
     desc = P.make_desc(1, 32, 8, 128, block=2048, dtype=torch.bfloat16, rope_base=1e6)
     assert P.workspace_bytes(desc) > 0
     _run_and_check(cfg, cuda)
+
+
+def test_c3_rope_full_batch(cuda):
+    """The bench's rotary launch at its full size (c3's batch of 256 and 2 GiB of pre-filled
+    rings, so the non-temporal kernel variant the bench times): every sequence against the
+    oracle at the first and last step of an 8-step run, taken 32 sequences at a time; the value
+    ring bit for bit and the key ring within one bf16 rounding of the exact rotation."""
+    cfg = W.get_config("c3").with_(rope_base=1e6, name="c3-rope-1e6")
+    steps, checks, chunk = 8, (0, 7), 32
+    t0 = W.initial_positions(cfg)
+    print(f"[rope] {cfg.name} batch={cfg.batch} steps={steps}", flush=True)
+    run = Run(cfg, t0, steps, cuda)
+    kept = {}
+    for i in range(steps):
+        q, out = run.step()
+        if i in checks:
+            kept[i] = (q.clone(), out.clone())
+    torch.cuda.synchronize()
+    stats = None
+    for c0 in range(0, cfg.batch, chunk):
+        rows = np.arange(c0, min(cfg.batch, c0 + chunk))
+        hist = run.history(rows, steps - 1)
+        for i in checks:
+            q, out = kept[i]
+            ref = run.oracle_out(rows, i, q, hist=hist)
+            got = to_np(out[torch.as_tensor(rows, device=cuda)])
+            compare(cfg, got, ref, what=f"{cfg.name} step {i} sequences {c0}..")
+            stats = merge_stats(stats, error_stats(got, ref), where=(i, c0))
+        exp_v = run.expected_ring(rows, steps - 1, "v", hist=hist)
+        assert np.array_equal(run.ring_rows(rows, "v"), exp_v), f"value ring, sequences {c0}.."
+        _check_keys(run, rows, steps - 1, hist)
+        del hist
+        run.__dict__.pop("_bits_cache", None)
+    stats.update(batch=cfg.batch, steps=steps, checked_steps=list(checks))
+    record_stats(cfg.name, stats)
