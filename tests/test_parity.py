@@ -173,6 +173,16 @@ def test_c5_swa_full_batch(cuda):
     _full_batch(W.get_config("c5"), cuda, strict=2e-2)
 
 
+@pytest.mark.parametrize("slots", [4096, 2048])
+def test_c5_paper_window_full_size_sampled(cuda, slots):
+    """The bench's paper-matched SWA rows at full size: c3's tensors and positions with the
+    window W = B = 2048 in 4096 slots (the paper's 2x buffer) and in 2048 slots (a B-slot ring);
+    the edge sequences and a sample of others at every one of 3 steps, rings bit for bit."""
+    cfg = W.get_config("c5").with_(window=2048, slots=slots, name=f"c5-w2048-s{slots}")
+    _, _, _, worst = _sampled(cfg, cuda, steps=3)
+    print(f"{cfg.name} {worst}")
+
+
 def test_c3_edge_rows_every_step(cuda):
     """c3 with forced edge positions: the edge sequences and a sample of others at every one
     of 3 consecutive steps (the full-batch test checks every sequence at 3 steps of a run)."""
