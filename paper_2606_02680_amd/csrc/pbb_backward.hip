@@ -316,7 +316,7 @@ void bwd_dkdv_kernel(BackwardArgs a, int tiles) {
   constexpr int NG = 32 / RPI;
   constexpr int TILE = 32 * ROWB;
   constexpr int BUF = 2 * TILE + 256;   // Q tile, dout tile, lse2[32] and -delta[32]
-  constexpr int STAGES = 3;
+  constexpr int STAGES = 4;              // two stages of two target steps each
   constexpr int ROWOPS = 2 * NG;        // row DMAs per step; wave 0 also issues the lse/delta one
   constexpr int MYOPS = ROWOPS / NW;
   static_assert(ROWOPS % NW == 0 && MYOPS >= 1, "DMA split");
@@ -434,7 +434,7 @@ void bwd_dkdv_kernel(BackwardArgs a, int tiles) {
     }
   const float c = a.scale_log2;
 
-  // Issue cursor (head, step) two steps ahead of the step being computed.
+  // Issue cursor (head, step): the next target step to load.
   int ih = 0, ij = 0;
   auto advance = [&]() {
     if (++ij == qsteps) {
@@ -448,25 +448,26 @@ void bwd_dkdv_kernel(BackwardArgs a, int tiles) {
     issue(1, ih, ij);
     advance();
   }
-  int rstage = 0;
 
   auto step = [&](int gs, int j, auto masked) {
-    if (wave == 0) {
-      if (gs + 1 < nsteps)
-        __builtin_amdgcn_s_waitcnt(0x0F70 | ((MYOPS + 1) & 15) | (((MYOPS + 1) >> 4) << 14));
-      else
-        __builtin_amdgcn_s_waitcnt(0x0F70);
-    } else {
-      if (gs + 1 < nsteps)
-        __builtin_amdgcn_s_waitcnt(0x0F70 | (MYOPS & 15) | ((MYOPS >> 4) << 14));
-      else
-        __builtin_amdgcn_s_waitcnt(0x0F70);
+    // Target steps go in pairs (buffers 0-1 and 2-3): at the start of a pair this wave's loads
+    // of both steps have landed; one barrier makes every wave's share visible and frees the
+    // other pair's buffers (every wave has finished the previous pair), and the next pair is
+    // issued into them -- one barrier per two steps (measured 2-4 % faster than one per step).
+    if ((gs & 1) == 0) {
+      __builtin_amdgcn_s_waitcnt(0x0F70);
+      lds_barrier();
+      const int ob = ((gs >> 1) & 1) ? 0 : 2;
+      if (gs + 2 < nsteps) {
+        issue(ob, ih, ij);
+        advance();
+      }
+      if (gs + 3 < nsteps) {
+        issue(ob + 1, ih, ij);
+        advance();
+      }
     }
-    lds_barrier();
-    if (gs + 2 < nsteps) {
-      issue(rstage == 0 ? 2 : rstage - 1, ih, ij);
-      advance();
-    }
+    const int rstage = ((gs >> 1) & 1) * 2 + (gs & 1);
     __builtin_amdgcn_sched_barrier(0);
     const uint32_t sb = (uint32_t)(rstage * BUF);
     const int q0 = q_first + 32 * j;
@@ -571,7 +572,6 @@ void bwd_dkdv_kernel(BackwardArgs a, int tiles) {
         acck[kc][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, w),
                                                                dsB[kc], acck[kc][nb], 0, 0, 0);
     }
-    rstage = rstage == STAGES - 1 ? 0 : rstage + 1;
     __builtin_amdgcn_sched_barrier(0);
   };
 
