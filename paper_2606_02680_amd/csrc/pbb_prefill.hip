@@ -39,6 +39,8 @@ constexpr int kPrefillColGroups64 = 2;
 
 // Starting reference of the running maximum (log2 units): finite and below any score.
 constexpr float kNoScore = -1.0e30f;
+// Largest sum of one lane's eight weights of a column a step keeps without moving m: 2^64.
+constexpr float kWeightCap = 18446744073709551616.0f;
 
 __device__ __forceinline__ int support_lo(const PrefillArgs& a, int t) {
   return support_start(a.mode, a.block, a.window, t);
@@ -225,63 +227,69 @@ void prefill_bf16_kernel(PrefillArgs a, int tq, int tiles) {
         s1[qc] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kb, qB[qc][kk], s1[qc], 0, 0, 0);
       }
     }
-    // Online softmax in log2 units with a lazily moved reference: m only moves (and the
-    // accumulators are rescaled) when some column's maximum exceeds it by more than 8, so that
-    // most steps skip the rescale and the weights stay <= 2^8.  The result is the same softmax:
-    // numerator and denominator share every reference change.
-    // A column's maximum exceeds m + 8 only if the maximum of one of its four lanes does, so
-    // the cross-lane reduction runs only in steps where some lane's own maximum does.
+    // Online softmax in log2 units with a lazily moved reference m (the log-sum-exp rescaling
+    // of Eq.(lse)): the weights are taken against the current m, and m moves to the column
+    // maxima (the accumulators rescaled, the weights taken again) only in a step where the
+    // eight weights of some lane and column sum above 2^64 or to infinity: a column's first
+    // step with a real score (m starts at a finite floor), and any step in which a score rises
+    // more than 64 log2 units above m.  No other step computes a maximum.  The result is the
+    // same softmax (numerator and denominator share every reference change), and the weights
+    // that enter the sums and products stay <= 2^64: finite in bf16 and fp32, with room for
+    // the sums.
     const float c = a.scale_log2;
     bf16x8 pB[QC];
-    float mx[QC];
-    bool over = false;
+    float ps[QC];
+    if constexpr (decltype(masked)::value) {
 #pragma unroll
-    for (int qc = 0; qc < QC; ++qc) {
-      mx[qc] = kNegInf;
+      for (int qc = 0; qc < QC; ++qc)
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        float sc = e < 4 ? s0[qc][e] : s1[qc][e - 4];
-        if constexpr (decltype(masked)::value) {
+        for (int e = 0; e < 8; ++e) {
           const int key = k0 + (e < 4 ? 4 * j4 + e : 16 + 4 * j4 + (e - 4));
-          sc = (key >= lo_c[qc] && key <= hi_c[qc]) ? sc : kNegInf;
-          if (e < 4) s0[qc][e] = sc; else s1[qc][e - 4] = sc;
+          const bool in = key >= lo_c[qc] && key <= hi_c[qc];
+          if (e < 4) s0[qc][e] = in ? s0[qc][e] : kNegInf;
+          else s1[qc][e - 4] = in ? s1[qc][e - 4] : kNegInf;
         }
-        mx[qc] = fmaxf(mx[qc], sc);
-      }
-      over |= mx[qc] * c > m[qc] + 8.0f;
     }
-    if (__builtin_amdgcn_ballot_w64(over) != 0) {
-      float alpha[QC];
-      bool grow_any = false;
+    auto weights = [&]() {
+      bool over = false;
 #pragma unroll
       for (int qc = 0; qc < QC; ++qc) {
-        const float cand = max_xor16_32(mx[qc]) * c;
-        const bool grow = cand > m[qc] + 8.0f;
-        alpha[qc] = grow ? fast_exp2(m[qc] - cand) : 1.0f;
-        m[qc] = grow ? cand : m[qc];
-        grow_any |= grow;
-      }
-      if (__builtin_amdgcn_ballot_w64(grow_any) != 0) {
+        float sum = 0.0f;
 #pragma unroll
-        for (int qc = 0; qc < QC; ++qc) {
-          lsum[qc] *= alpha[qc];
-#pragma unroll
-          for (int nb = 0; nb < NB; ++nb) acc[qc][nb] *= alpha[qc];
+        for (int e = 0; e < 8; ++e) {
+          const float sc = e < 4 ? s0[qc][e] : s1[qc][e - 4];
+          const float pe = fast_exp2(__builtin_fmaf(sc, c, -m[qc]));
+          sum += pe;
+          pB[qc][e] = (__bf16)pe;
         }
+        ps[qc] = sum;
+        over |= !(sum <= kWeightCap);
       }
+      return over;
+    };
+    auto move_reference = [&]() {
+#pragma unroll
+      for (int qc = 0; qc < QC; ++qc) {
+        float mx = kNegInf;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) mx = fmaxf(mx, e < 4 ? s0[qc][e] : s1[qc][e - 4]);
+        const float cand = max_xor16_32(mx) * c;
+        const bool grow = cand > m[qc];
+        const float alpha = grow ? fast_exp2(m[qc] - cand) : 1.0f;
+        m[qc] = grow ? cand : m[qc];
+        lsum[qc] *= alpha;
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) acc[qc][nb] *= alpha;
+      }
+    };
+    // The first step sets the reference before its weights (it would always move it).
+    if (st == 0) move_reference();
+    if (__builtin_amdgcn_ballot_w64(weights()) != 0) {
+      move_reference();
+      weights();
     }
 #pragma unroll
-    for (int qc = 0; qc < QC; ++qc) {
-      float ps = 0.0f;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float sc = e < 4 ? s0[qc][e] : s1[qc][e - 4];
-        const float pe = fast_exp2(__builtin_fmaf(sc, c, -m[qc]));
-        ps += pe;
-        pB[qc][e] = (__bf16)pe;
-      }
-      lsum[qc] += ps;
-    }
+    for (int qc = 0; qc < QC; ++qc) lsum[qc] += ps[qc];
     // V^T operand of O^T += V^T P^T: lane (c16, j4) needs channel 16nb + c16 of keys
     // 4j4..4j4+3 and 16+4j4..16+4j4+3 (the key order of P^T in the score layout).  One
     // transposed read per half: within each 16-lane group, lane i names 4 channels
