@@ -15,6 +15,11 @@ typedef __attribute__((ext_vector_type(2))) unsigned int u32x2;
 constexpr int kCachePolicyNT = 2;
 
 constexpr float kNegInf = -__builtin_huge_valf();
+// Largest sum of one lane's eight softmax weights of a column that a key step keeps without
+// moving its reference: 2^8, so every weight stays <= 2^8, and a key whose score rises more
+// than 8 log2 units above the reference (the usual dominant key of a peaked row) becomes the
+// new reference and enters with weight exactly 1, unrounded.
+constexpr float kWeightCap = 256.0f;
 
 // float -> bf16 with round-to-nearest-even (inputs are finite).
 __device__ __forceinline__ uint16_t float_to_bf16_rne(float f) {

@@ -710,6 +710,7 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
   bf16x8 qB[KK];
   float m = kNegInf;
   float lsum = 0.0f;
+  bool fresh = true;  // no step computed yet by this wave
   f32x4 acc[NB];
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
@@ -856,29 +857,45 @@ __global__ __launch_bounds__(NW * 64) void decode_bf16_kernel(DecodeArgs a) {
         }
       }
     }
-    float mx = fmaxf(fmaxf(fmaxf(s0[0], s0[1]), fmaxf(s0[2], s0[3])),
-                     fmaxf(fmaxf(s1[0], s1[1]), fmaxf(s1[2], s1[3])));
-    mx = max_xor16_32(mx);
-    const float cand = mx * c;
-    const bool grow = cand > m + 8.0f;
-    if (__builtin_amdgcn_ballot_w64(grow) != 0) {
+    // Online softmax with a lazily moved reference m (Eq.(lse) rescaling): a wave's first step
+    // sets m to its columns' maxima; later steps take their weights against m and move it (the
+    // accumulators rescaled, the weights taken again) only when the eight weights of some lane
+    // sum above 2^8 or to infinity -- whenever a score rises more than 8 log2 units above m,
+    // and when several rise more than 5 -- so no other step computes a maximum.  Numerator and
+    // denominator share every reference; the weights that enter them stay <= 2^8.
+    auto move_reference = [&]() {
+      float mx = fmaxf(fmaxf(fmaxf(s0[0], s0[1]), fmaxf(s0[2], s0[3])),
+                       fmaxf(fmaxf(s1[0], s1[1]), fmaxf(s1[2], s1[3])));
+      const float cand = max_xor16_32(mx) * c;
+      const bool grow = cand > m;
       const float alpha = grow ? fast_exp2(m - cand) : 1.0f;   // 0 on the first step
       m = grow ? cand : m;
       lsum *= alpha;
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) acc[nb] *= alpha;
-    }
+    };
     // The weights enter the value product rounded to bf16; the denominator sums the same
     // rounded weights, so the output is an exactly normalised average of the values under
     // those weights.  (Summing the unrounded weights instead leaves a mismatch of up to 2^-9
     // relative that scales with |o| itself, e.g. when one key carries almost all the weight.)
-    float ps = 0.0f;
+    float ps;
     bf16x8 pB;
+    auto weights = [&]() {
+      float sum = 0.0f;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float sc = e < 4 ? s0[e] : s1[e - 4];
-      pB[e] = (__bf16)fast_exp2(__builtin_fmaf(sc, c, -m));
-      ps += (float)pB[e];
+      for (int e = 0; e < 8; ++e) {
+        const float sc = e < 4 ? s0[e] : s1[e - 4];
+        pB[e] = (__bf16)fast_exp2(__builtin_fmaf(sc, c, -m));
+        sum += (float)pB[e];
+      }
+      ps = sum;
+      return !(sum <= kWeightCap);
+    };
+    if (fresh) move_reference();
+    fresh = false;
+    if (__builtin_amdgcn_ballot_w64(weights()) != 0) {
+      move_reference();
+      weights();
     }
     lsum += ps;
     if constexpr (NB == 8) {

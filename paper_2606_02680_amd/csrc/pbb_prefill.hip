@@ -39,8 +39,6 @@ constexpr int kPrefillColGroups64 = 2;
 
 // Starting reference of the running maximum (log2 units): finite and below any score.
 constexpr float kNoScore = -1.0e30f;
-// Largest sum of one lane's eight weights of a column a step keeps without moving m: 2^64.
-constexpr float kWeightCap = 18446744073709551616.0f;
 
 __device__ __forceinline__ int support_lo(const PrefillArgs& a, int t) {
   return support_start(a.mode, a.block, a.window, t);
@@ -230,12 +228,11 @@ void prefill_bf16_kernel(PrefillArgs a, int tq, int tiles) {
     // Online softmax in log2 units with a lazily moved reference m (the log-sum-exp rescaling
     // of Eq.(lse)): the weights are taken against the current m, and m moves to the column
     // maxima (the accumulators rescaled, the weights taken again) only in a step where the
-    // eight weights of some lane and column sum above 2^64 or to infinity: a column's first
-    // step with a real score (m starts at a finite floor), and any step in which a score rises
-    // more than 64 log2 units above m.  No other step computes a maximum.  The result is the
-    // same softmax (numerator and denominator share every reference change), and the weights
-    // that enter the sums and products stay <= 2^64: finite in bf16 and fp32, with room for
-    // the sums.
+    // eight weights of some lane and column sum above 2^8 or to infinity: a column's first
+    // step with a real score (m starts at a finite floor), any step in which a score rises
+    // more than 8 log2 units above m, and steps where several rise more than 5.  No other step
+    // computes a maximum.  The result is the same softmax (numerator and denominator share
+    // every reference change), and the weights that enter the sums and products stay <= 2^8.
     const float c = a.scale_log2;
     bf16x8 pB[QC];
     float ps[QC];

@@ -112,20 +112,20 @@ def test_prefill_without_optional_outputs(cuda):
     ("swa", 1, 500, 8, 2, 128, 0, 100, 128),
 ])
 def test_prefill_rising_scores(cuda, mode, batch, n, hq, hkv, d, block, window, slots):
-    """Scores that jump far above everything the walk has seen: every query carries 8 in
-    channel 0 and a few keys carry a boost there worth about 40 or about 100 log2 units of
-    score (3 % and 2 % of keys), so within most tiles the softmax's dominant keys first appear
-    after the first key step.  Rises under 64 log2 units keep the softmax reference and enter
-    the sums with weights up to ~2^40; larger ones move it mid-walk.  Outputs (dominated by
-    the boosted keys' values) and log-partitions (~70 in natural-log units) against the
-    oracle on the same bf16 inputs."""
+    """Scores that jump above everything the walk has seen: every query carries 8 in channel 0
+    and a few keys carry a boost there worth about 4 or about 40 log2 units of score (3 % and
+    2 % of keys), so within most tiles the softmax's dominant keys first appear after the first
+    key step.  Small rises keep the softmax reference (weights up to ~2^4); large ones move it
+    mid-walk, the dominant key becoming the reference.  Outputs (dominated by the boosted keys'
+    values) and log-partitions (up to ~30 in natural-log units) against the oracle on the same
+    bf16 inputs."""
     cfg = _cfg(mode, batch, n, hq, hkv, d, block, window, slots, seed=53)
     q, k, v = W.prompt(cfg, n, device=cuda)
     c = np.log2(np.e) / np.sqrt(d)                      # log2 units per unit of q.k
-    b40, b100 = float(round(40 / (8 * c))), float(round(100 / (8 * c)))
+    b4, b40 = float(round(4 / (8 * c))), float(round(40 / (8 * c)))
     g = torch.Generator().manual_seed(1234)
     u = torch.rand((batch, n, hkv), generator=g)
-    boost = torch.where(u < 0.03, b40, torch.where(u < 0.05, b100, 0.0))
+    boost = torch.where(u < 0.03, b4, torch.where(u < 0.05, b40, 0.0))
     q[..., 0] = 8.0
     k[..., 0] = boost.to(device=cuda, dtype=k.dtype)
     desc = _desc(cfg)
@@ -137,7 +137,7 @@ def test_prefill_rising_scores(cuda, mode, batch, n, hq, hkv, d, block, window, 
     torch.cuda.synchronize()
     m = oracle.SWA if mode == "swa" else oracle.PBB
     ref, ref_lse = oracle.prefill(m, to_np(q), to_np(k), to_np(v), block=block, window=window)
-    assert ref_lse.max() > 60.0                         # the boosts dominate where present
+    assert ref_lse.max() > 25.0                         # the boosts dominate where present
     compare(cfg, to_np(out), ref, what=f"rising scores {cfg.name}")
     got_lse = lse.cpu().numpy().astype(np.float64)
     assert np.isfinite(got_lse).all()
