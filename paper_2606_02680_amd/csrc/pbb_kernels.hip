@@ -474,11 +474,11 @@ void decode_f32_mfma_kernel(DecodeArgs a) {
 //           operand (lane l: key l%16, channels 32kk + 8(l/16) .. +7) is one 16-byte LDS read,
 //           the B operand holds the group's queries, padded to 16 heads with zeros.
 //   softmax lane (head h = l%16, quarter j = l/16) holds the scores of keys 4j..4j+3 and
-//           16+4j..16+4j+3; the column maximum is shared across the four quarters with
-//           permlane swaps.  The reference maximum moves (and the accumulators are rescaled)
-//           only when some head's maximum exceeds it by more than 8 in log2 units, decided
-//           wave-uniformly, so most steps skip the rescale; weights stay <= 2^8 and numerator
-//           and denominator share every reference (the same softmax).
+//           16+4j..16+4j+3.  A wave's first step sets the reference to the heads' maxima
+//           (shared across the four quarters with permlane swaps); later steps compute no
+//           maximum: the reference moves (and the accumulators are rescaled) only when some
+//           lane's weights sum above 2^8, decided wave-uniformly, so weights stay <= 2^8 and
+//           numerator and denominator share every reference (the same softmax).
 //   values  O^T[16 channels][16 heads] += V^T P^T.  P^T's B operand is exactly the score
 //           registers (rounded to bf16); V^T comes from transposed LDS reads
 //           (ds_read_b64_tr_b16: lane i of each 16-lane group names 4 channels of key row
