@@ -761,8 +761,8 @@ def main(argv=None):
                     help="time the steps as eager back-to-back launches instead of a HIP graph")
     args = ap.parse_args(argv)
     if args.gpus != 1:
-        print(f"bench.py: this build measures one GPU only; --gpus {args.gpus} is not supported "
-              "(the decode core shards by sequence or KV head with no exchange; see DESIGN.md)",
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported (the decode "
+              "core shards by sequence or KV head with no exchange between GPUs)",
               file=sys.stderr)
         return 2
 

@@ -152,7 +152,7 @@ def _full_batch(cfg, device, steps=128, checks=(0, 64, 127), chunk=32, strict=No
 
 def test_c3_full_batch(cuda):
     """c3 (batch 256, Hq 32, Hkv 8, d 128, B 2048): all 256 sequences at steps 0, 64, 127;
-    outputs here are small (|o| < 2), so the benchmark spec's plain 2e-2 max-abs is asserted too."""
+    outputs here are small (|o| < 2), so the plain 2e-2 max-abs bound is asserted too."""
     _full_batch(W.get_config("c3"), cuda, strict=2e-2)
 
 
